@@ -1,0 +1,195 @@
+"""float64 CPU oracle for the block-sparse linear layer (LPViT, arXiv 2407.02068).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+CPU-baseline leg of ``bench.py`` may import this package.  It shares no code
+with the GPU library (``paper_2407_02068_amd``) and imports nothing from it.
+
+It is a thin ctypes binding over ``liblpv_oracle.so`` (``lpv_oracle.c``), which
+computes the paper's masked weight (Sec. 3.1) and the linear layer
+``Y = g(X W~^T + b)`` in float64; see that file's header for the definitions.
+
+Element types are given by name: ``"f32"`` (numpy float32 arrays), ``"f16"``
+(numpy float16) and ``"bf16"`` (numpy uint16 arrays holding the bf16 bit
+patterns).
+"""
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "liblpv_oracle.so")
+_CODES = {"f32": 0, "f16": 1, "bf16": 2}
+_NP = {"f32": np.float32, "f16": np.float16, "bf16": np.uint16}
+
+
+class Oracle:
+    """Binding to one build of the oracle library (the default build, or a
+    copy the tests compiled elsewhere)."""
+
+    def __init__(self, path=_LIB_PATH):
+        if path == _LIB_PATH and not os.path.exists(path):
+            from . import build as _build  # plain C: build it on demand
+            _build.build()
+        lib = ctypes.CDLL(path)
+        i64, i32, vp = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+        lib.lpvo_elem_size.argtypes = [i32]
+        lib.lpvo_elem_size.restype = i32
+        lib.lpvo_decode.argtypes = [i32, vp, i64, vp]
+        lib.lpvo_decode.restype = i32
+        lib.lpvo_pack.argtypes = [i32, vp, i64, i64, i64, i32, i32, vp, vp, vp, vp]
+        lib.lpvo_pack.restype = i64
+        lib.lpvo_unpack.argtypes = [i32, i64, i64, i32, i32, vp, vp, vp, vp, i64]
+        lib.lpvo_unpack.restype = i32
+        lib.lpvo_gelu.argtypes = [ctypes.c_double]
+        lib.lpvo_gelu.restype = ctypes.c_double
+        lib.lpvo_linear.argtypes = [i32, vp, i64, i64, vp, i64, i64, i64, i32, i32, vp, vp,
+                                    i32, vp, i64, i32]
+        lib.lpvo_linear.restype = i32
+        self.lib = lib
+        self.path = path
+
+    def decode(self, arr, dtype):
+        """Exact float64 value of every element of ``arr`` (same shape)."""
+        arr = np.ascontiguousarray(arr)
+        _check(arr, dtype, "arr")
+        out = np.empty(arr.shape, np.float64)
+        if self.lib.lpvo_decode(_CODES[dtype], _ptr(arr), arr.size, _ptr(out)):
+            raise ValueError("lpvo_decode failed")
+        return out
+
+    def gelu(self, v):
+        """Exact-erf GELU in float64 (scalar)."""
+        return self.lib.lpvo_gelu(float(v))
+
+    def pack(self, W, dtype, b_r, b_c, mask):
+        """Plain BSR pack: ``(row_ptr int32[R+1], col_idx int32[nnzb],
+        values[nnzb, b_r, b_c])``; ``values`` has W's numpy type and holds the
+        raw element bits of each kept block, row-major."""
+        W = np.ascontiguousarray(W)
+        _check(W, dtype, "W")
+        mask = np.ascontiguousarray(mask, dtype=np.uint8)
+        N, K = W.shape
+        if b_r <= 0 or b_c <= 0 or N % b_r or K % b_c:
+            raise ValueError("block %dx%d does not divide weight %dx%d" % (b_r, b_c, N, K))
+        R, C = N // b_r, K // b_c
+        if mask.shape != (R, C):
+            raise ValueError("mask shape %s, expected %s" % (mask.shape, (R, C)))
+        code = _CODES[dtype]
+        nnzb = self.lib.lpvo_pack(code, _ptr(W), K, N, K, b_r, b_c, _ptr(mask), None, None, None)
+        if nnzb < 0:
+            raise ValueError("lpvo_pack rejected its arguments")
+        row_ptr = np.zeros(R + 1, np.int32)
+        col_idx = np.zeros(nnzb, np.int32)
+        values = np.zeros((nnzb, b_r, b_c), W.dtype)
+        got = self.lib.lpvo_pack(code, _ptr(W), K, N, K, b_r, b_c, _ptr(mask), _ptr(row_ptr),
+                                 _ptr(col_idx), _ptr(values))
+        if got != nnzb:
+            raise RuntimeError("lpvo_pack returned %d then %d blocks" % (nnzb, got))
+        return row_ptr, col_idx, values
+
+    def unpack(self, row_ptr, col_idx, values, dtype, N, K, b_r, b_c):
+        """Inverse of :meth:`pack`: the pruned dense weight (N x K), +0.0 in
+        dropped blocks."""
+        row_ptr = np.ascontiguousarray(row_ptr, dtype=np.int32)
+        col_idx = np.ascontiguousarray(col_idx, dtype=np.int32)
+        values = np.ascontiguousarray(values)
+        _check(values, dtype, "values")
+        out = np.empty((N, K), _NP[dtype])
+        if self.lib.lpvo_unpack(_CODES[dtype], N, K, b_r, b_c, _ptr(row_ptr), _ptr(col_idx),
+                                _ptr(values), _ptr(out), K):
+            raise ValueError("lpvo_unpack rejected its arguments")
+        return out
+
+    def linear(self, X, W, dtype, b_r, b_c, mask, bias=None, gelu=False, nthreads=None):
+        """``Y = g(X W~^T + b)`` in float64 (M x N), not rounded."""
+        X = np.ascontiguousarray(X)
+        W = np.ascontiguousarray(W)
+        _check(X, dtype, "X")
+        _check(W, dtype, "W")
+        mask = np.ascontiguousarray(mask, dtype=np.uint8)
+        M, K = X.shape
+        N, K2 = W.shape
+        if K2 != K:
+            raise ValueError("X is %dx%d but W is %dx%d" % (M, K, N, K2))
+        if b_r <= 0 or b_c <= 0 or N % b_r or K % b_c:
+            raise ValueError("block %dx%d does not divide weight %dx%d" % (b_r, b_c, N, K))
+        if mask.shape != (N // b_r, K // b_c):
+            raise ValueError("mask shape %s, expected %s" % (mask.shape, (N // b_r, K // b_c)))
+        if bias is not None:
+            bias = np.ascontiguousarray(bias)
+            _check(bias, dtype, "bias")
+            if bias.shape != (N,):
+                raise ValueError("bias shape %s, expected (%d,)" % (bias.shape, N))
+        Y = np.empty((M, N), np.float64)
+        nt = default_threads() if nthreads is None else int(nthreads)
+        rc = self.lib.lpvo_linear(_CODES[dtype], _ptr(X), K, M, _ptr(W), K, N, K, b_r, b_c,
+                                  _ptr(mask), _ptr(bias), 1 if gelu else 0, _ptr(Y), N, nt)
+        if rc:
+            raise RuntimeError("lpvo_linear failed (%d)" % rc)
+        return Y
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _check(arr, dtype, name):
+    if dtype not in _CODES:
+        raise ValueError("unknown element type %r" % (dtype,))
+    if arr.dtype != _NP[dtype]:
+        raise TypeError("%s: expected numpy %s for %s, got %s"
+                        % (name, np.dtype(_NP[dtype]).name, dtype, arr.dtype))
+    if not arr.flags.c_contiguous:
+        raise ValueError("%s must be C-contiguous" % name)
+
+
+def default_threads():
+    """Host threads this process may run on."""
+    try:
+        return len(os.sched_getaffinity(0))
+    except AttributeError:  # pragma: no cover
+        return os.cpu_count() or 1
+
+
+_default = None
+
+
+def default():
+    """The oracle built from ``lpv_oracle.c`` next to this file."""
+    global _default
+    if _default is None:
+        _default = Oracle()
+    return _default
+
+
+def decode(arr, dtype):
+    return default().decode(arr, dtype)
+
+
+def gelu(v):
+    return default().gelu(v)
+
+
+def pack(W, dtype, b_r, b_c, mask):
+    return default().pack(W, dtype, b_r, b_c, mask)
+
+
+def unpack(row_ptr, col_idx, values, dtype, N, K, b_r, b_c):
+    return default().unpack(row_ptr, col_idx, values, dtype, N, K, b_r, b_c)
+
+
+def linear(X, W, dtype, b_r, b_c, mask, bias=None, gelu=False, nthreads=None):
+    return default().linear(X, W, dtype, b_r, b_c, mask, bias, gelu, nthreads)
+
+
+def rel_err(y, ref):
+    """Infinity-norm relative error ``max|y - r| / max|r|`` (float64); when the
+    reference is all zero, 0.0 if ``y`` is exactly zero too, else inf."""
+    y = np.asarray(y, np.float64)
+    ref = np.asarray(ref, np.float64)
+    scale = np.max(np.abs(ref)) if ref.size else 0.0
+    diff = np.max(np.abs(y - ref)) if ref.size else 0.0
+    if scale == 0.0:
+        return 0.0 if diff == 0.0 else float("inf")
+    return float(diff / scale)

@@ -1,0 +1,311 @@
+/*
+ * lpv_oracle.c -- float64 CPU oracle for the block-sparse linear layer of
+ * LPViT (arXiv 2407.02068).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the slow, plain definition that the
+ * GPU library is checked against.  Only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark may load it.  It shares no source, header,
+ * table or helper with the HIP library, and it includes nothing from it.
+ *
+ * What it computes (paper, Sec. 3.1, the masked-weight formula):
+ *   A weight W (H x W in the paper, N x K here: output features x input
+ *   features, the nn.Linear layout) is cut into a grid of fixed (B_h, B_w)
+ *   blocks; a binary block mask M keeps or drops each block, and the pruned
+ *   weight is W~[i][j] = W[i][j] * M[ceil(i/B_h)][ceil(j/B_w)] (1-based).  With
+ *   0-based indices the block of element (n, k) is (n / b_r, k / b_c), where
+ *   b_r = B_h runs along output features and b_c = B_w along the reduction.
+ *   The grid S' has H/B_h x W/B_w entries, so the block sizes must divide the
+ *   weight's sides exactly (same passage); other shapes are rejected.
+ *
+ *   Pruning is applied here by SELECTION: a dropped element is replaced by
+ *   0.0, it is not multiplied by 0.  A NaN or Inf stored in a dropped block
+ *   therefore never reaches the output.
+ *
+ *   The linear layer is Y = X * W~^T + b over tokens m (rows of X), with an
+ *   optional exact-erf GELU after the bias, all in float64:
+ *     Y[m][n] = g( sum_{k=0}^{K-1} X[m][k] * W~[n][k] + b[n] ),
+ *   g = identity or g(v) = v/2 * (1 + erf(v / sqrt 2)).
+ *   The sum runs over k in ascending order.  Nothing is rounded to a narrower
+ *   type: the float64 result is returned as is.
+ *
+ *   The BSR (block compressed sparse row) arrays that the library's pack call
+ *   must reproduce bit for bit are, in the oracle's own plain form:
+ *     row_ptr[0] = 0, row_ptr[r+1] = row_ptr[r] + (number of kept blocks in
+ *       block-row r);
+ *     col_idx[row_ptr[r] .. row_ptr[r+1]) = the kept block columns of block-row
+ *       r in ascending order;
+ *     values[p] = the raw element bits of kept block p, b_r rows of b_c
+ *       elements, row-major.
+ *   The kept count of a weight is the paper's per-matmul block count in its
+ *   power model (Sec. 3.4): the number of blocks that survive pruning.
+ *
+ * Element types: 0 = fp32, 1 = fp16 (IEEE binary16), 2 = bf16.  Inputs are
+ * decoded exactly to float64 by the decoders below, written from the IEEE 754
+ * definitions of the formats.
+ *
+ * Build: gcc -O2 -ffp-contract=off -fno-fast-math -fPIC -shared -pthread
+ *        lpv_oracle.c -o liblpv_oracle.so -lm
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include "lpv_oracle.h"
+
+/* ------------------------------------------------------------------------ */
+/* Exact decoders                                                            */
+/* ------------------------------------------------------------------------ */
+
+/* bf16 is the upper half of an IEEE binary32: append 16 zero bits. */
+static double dec_bf16(uint16_t b)
+{
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+/* IEEE binary16: 1 sign bit, 5 exponent bits (bias 15), 10 fraction bits. */
+static double dec_f16(uint16_t h)
+{
+    int sign = (h >> 15) & 1;
+    int e = (h >> 10) & 0x1f;
+    int f = h & 0x3ff;
+    double v;
+    if (e == 0)
+        v = ldexp((double)f, -24); /* subnormal: f * 2^-14 / 2^10 */
+    else if (e == 31)
+        v = f ? NAN : INFINITY;
+    else
+        v = ldexp((double)(1024 + f), e - 25); /* (1 + f/2^10) * 2^(e-15) */
+    return sign ? -v : v;
+}
+
+static double dec_f32(uint32_t u)
+{
+    float f;
+    memcpy(&f, &u, sizeof f);
+    return (double)f;
+}
+
+int lpvo_elem_size(int dtype)
+{
+    switch (dtype) {
+    case LPVO_F32: return 4;
+    case LPVO_F16: return 2;
+    case LPVO_BF16: return 2;
+    default: return 0;
+    }
+}
+
+static double dec_one(int dtype, const void* base, int64_t idx)
+{
+    if (dtype == LPVO_F32) {
+        uint32_t u;
+        memcpy(&u, (const char*)base + 4 * idx, 4);
+        return dec_f32(u);
+    }
+    uint16_t h;
+    memcpy(&h, (const char*)base + 2 * idx, 2);
+    return dtype == LPVO_F16 ? dec_f16(h) : dec_bf16(h);
+}
+
+int lpvo_decode(int dtype, const void* src, int64_t n, double* dst)
+{
+    if (!lpvo_elem_size(dtype) || n < 0 || (n > 0 && (!src || !dst)))
+        return -1;
+    for (int64_t i = 0; i < n; ++i)
+        dst[i] = dec_one(dtype, src, i);
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Block grid and BSR pack / unpack (Sec. 3.1)                               */
+/* ------------------------------------------------------------------------ */
+
+static int grid_ok(int64_t N, int64_t K, int b_r, int b_c)
+{
+    return N >= 0 && K >= 0 && b_r > 0 && b_c > 0 && N % b_r == 0 && K % b_c == 0;
+}
+
+int64_t lpvo_pack(int dtype, const void* W, int64_t ldw, int64_t N, int64_t K,
+                  int b_r, int b_c, const uint8_t* mask,
+                  int32_t* row_ptr, int32_t* col_idx, void* values)
+{
+    int es = lpvo_elem_size(dtype);
+    if (!es || !grid_ok(N, K, b_r, b_c) || ldw < K || !mask)
+        return -1;
+    int64_t R = N / b_r, C = K / b_c;
+    int64_t p = 0;
+    if (row_ptr)
+        row_ptr[0] = 0;
+    for (int64_t r = 0; r < R; ++r) {
+        for (int64_t c = 0; c < C; ++c) {
+            if (!mask[r * C + c])
+                continue;
+            if (col_idx)
+                col_idx[p] = (int32_t)c;
+            if (values) {
+                /* block p holds rows r*b_r.. and columns c*b_c.. of W */
+                char* dst = (char*)values + p * (int64_t)b_r * b_c * es;
+                for (int i = 0; i < b_r; ++i) {
+                    const char* src = (const char*)W + ((r * b_r + i) * ldw + c * b_c) * es;
+                    memcpy(dst + (int64_t)i * b_c * es, src, (size_t)b_c * es);
+                }
+            }
+            ++p;
+        }
+        if (row_ptr)
+            row_ptr[r + 1] = (int32_t)p;
+    }
+    return p;
+}
+
+int lpvo_unpack(int dtype, int64_t N, int64_t K, int b_r, int b_c,
+                const int32_t* row_ptr, const int32_t* col_idx, const void* values,
+                void* W_out, int64_t ldw)
+{
+    int es = lpvo_elem_size(dtype);
+    if (!es || !grid_ok(N, K, b_r, b_c) || ldw < K || !row_ptr || !W_out)
+        return -1;
+    int64_t R = N / b_r, C = K / b_c;
+    /* every element starts as +0.0, which is all-zero bits in all three formats */
+    for (int64_t n = 0; n < N; ++n)
+        memset((char*)W_out + n * ldw * es, 0, (size_t)K * es);
+    for (int64_t r = 0; r < R; ++r) {
+        for (int64_t p = row_ptr[r]; p < row_ptr[r + 1]; ++p) {
+            int64_t c = col_idx[p];
+            if (c < 0 || c >= C)
+                return -1;
+            const char* src = (const char*)values + p * (int64_t)b_r * b_c * es;
+            for (int i = 0; i < b_r; ++i) {
+                char* dst = (char*)W_out + ((r * b_r + i) * ldw + c * b_c) * es;
+                memcpy(dst, src + (int64_t)i * b_c * es, (size_t)b_c * es);
+            }
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------------------------------ */
+/* Y = g(X W~^T + b) in float64                                              */
+/* ------------------------------------------------------------------------ */
+
+double lpvo_gelu(double v)
+{
+    /* GELU(v) = v * Phi(v), Phi the standard normal CDF written with erf */
+    return 0.5 * v * (1.0 + erf(v / sqrt(2.0)));
+}
+
+struct linear_job {
+    int dtype;
+    const void* X;
+    int64_t ldx;
+    int64_t m_begin, m_end;
+    const double* Wt; /* [K][N]: the expanded, pruned weight, transposed */
+    const double* b;  /* [N] */
+    int64_t N, K;
+    int gelu;
+    double* Y;
+    int64_t ldy;
+};
+
+static void* linear_rows(void* arg)
+{
+    struct linear_job* j = (struct linear_job*)arg;
+    double* x = (double*)malloc(sizeof(double) * (size_t)(j->K ? j->K : 1));
+    double* acc = (double*)malloc(sizeof(double) * (size_t)(j->N ? j->N : 1));
+    if (!x || !acc) {
+        free(x);
+        free(acc);
+        return (void*)1;
+    }
+    for (int64_t m = j->m_begin; m < j->m_end; ++m) {
+        for (int64_t k = 0; k < j->K; ++k)
+            x[k] = dec_one(j->dtype, j->X, m * j->ldx + k);
+        for (int64_t n = 0; n < j->N; ++n)
+            acc[n] = 0.0;
+        /* acc[n] = sum over k ascending of X[m][k] * W~[n][k] */
+        for (int64_t k = 0; k < j->K; ++k) {
+            const double xk = x[k];
+            const double* wk = j->Wt + k * j->N;
+            for (int64_t n = 0; n < j->N; ++n)
+                acc[n] += xk * wk[n];
+        }
+        double* y = j->Y + m * j->ldy;
+        for (int64_t n = 0; n < j->N; ++n) {
+            double v = acc[n] + j->b[n];
+            y[n] = j->gelu ? lpvo_gelu(v) : v;
+        }
+    }
+    free(x);
+    free(acc);
+    return NULL;
+}
+
+int lpvo_linear(int dtype, const void* X, int64_t ldx, int64_t M,
+                const void* W, int64_t ldw, int64_t N, int64_t K,
+                int b_r, int b_c, const uint8_t* mask, const void* bias,
+                int gelu, double* Y, int64_t ldy, int nthreads)
+{
+    if (!lpvo_elem_size(dtype) || !grid_ok(N, K, b_r, b_c) || M < 0 || ldx < K ||
+        ldw < K || ldy < N || !mask || (M > 0 && (!X || !Y)) || (N * K > 0 && !W))
+        return -1;
+    if (M == 0 || N == 0)
+        return 0;
+    const int64_t C = K / b_c;
+    double* Wt = (double*)malloc(sizeof(double) * (size_t)(K * N + 1));
+    double* b = (double*)malloc(sizeof(double) * (size_t)N);
+    if (!Wt || !b) {
+        free(Wt);
+        free(b);
+        return -2;
+    }
+    /* Expand the block mask into the dense pruned weight, transposed. */
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k)
+            Wt[k * N + n] = mask[(n / b_r) * C + (k / b_c)] ? dec_one(dtype, W, n * ldw + k) : 0.0;
+    for (int64_t n = 0; n < N; ++n)
+        b[n] = bias ? dec_one(dtype, bias, n) : 0.0;
+
+    if (nthreads < 1)
+        nthreads = 1;
+    if (nthreads > M)
+        nthreads = (int)M;
+    struct linear_job* jobs = (struct linear_job*)calloc((size_t)nthreads, sizeof *jobs);
+    pthread_t* tid = (pthread_t*)calloc((size_t)nthreads, sizeof *tid);
+    char* running = (char*)calloc((size_t)nthreads, 1);
+    int rc = 0;
+    if (!jobs || !tid || !running) {
+        rc = -2;
+        goto out;
+    }
+    /* contiguous ranges of token rows, one per thread; each row is computed
+       entirely by one thread, so the result does not depend on nthreads */
+    for (int t = 0; t < nthreads; ++t) {
+        jobs[t] = (struct linear_job){dtype, X, ldx, M * t / nthreads, M * (t + 1) / nthreads,
+                                      Wt, b, N, K, gelu, Y, ldy};
+    }
+    for (int t = 1; t < nthreads; ++t)
+        running[t] = pthread_create(&tid[t], NULL, linear_rows, &jobs[t]) == 0;
+    for (int t = 0; t < nthreads; ++t)
+        if (!running[t] && linear_rows(&jobs[t]))
+            rc = -2;
+    for (int t = 1; t < nthreads; ++t) {
+        if (running[t]) {
+            void* ret = NULL;
+            pthread_join(tid[t], &ret);
+            if (ret)
+                rc = -2;
+        }
+    }
+out:
+    free(jobs);
+    free(tid);
+    free(running);
+    free(Wt);
+    free(b);
+    return rc;
+}

@@ -1,0 +1,52 @@
+/*
+ * lpv_oracle.h -- the float64 CPU oracle's own interface (test infrastructure
+ * only; see lpv_oracle.c).  It is independent of the library's include/lpv.h:
+ * the two declare no common type, constant or function.
+ */
+#ifndef LPV_ORACLE_H
+#define LPV_ORACLE_H
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { LPVO_F32 = 0, LPVO_F16 = 1, LPVO_BF16 = 2 };
+
+/* Bytes per element of an element type, 0 for an unknown type. */
+int lpvo_elem_size(int dtype);
+
+/* Exact decode of n elements to float64.  Returns 0, or -1 on a bad argument. */
+int lpvo_decode(int dtype, const void* src, int64_t n, double* dst);
+
+/* Plain BSR pack of W (N x K, row stride ldw elements) under the row-major
+ * block mask (N/b_r x K/b_c).  row_ptr, col_idx and values may each be NULL to
+ * skip that output.  Returns the kept-block count, or -1 on a bad argument
+ * (including block sizes that do not divide N or K). */
+int64_t lpvo_pack(int dtype, const void* W, int64_t ldw, int64_t N, int64_t K,
+                  int b_r, int b_c, const uint8_t* mask,
+                  int32_t* row_ptr, int32_t* col_idx, void* values);
+
+/* Inverse of lpvo_pack: writes the pruned dense weight, +0.0 in dropped
+ * blocks.  Returns 0, or -1 on a bad argument. */
+int lpvo_unpack(int dtype, int64_t N, int64_t K, int b_r, int b_c,
+                const int32_t* row_ptr, const int32_t* col_idx, const void* values,
+                void* W_out, int64_t ldw);
+
+/* GELU with the exact error function, float64. */
+double lpvo_gelu(double v);
+
+/* Y (float64, M x N, row stride ldy) = g(X W~^T + b); X is M x K (row stride
+ * ldx), W is N x K (row stride ldw), bias has N elements or is NULL, all of
+ * element type dtype.  gelu != 0 selects g = GELU.  Rows of Y are split over
+ * nthreads host threads.  Returns 0, -1 on a bad argument, -2 when host memory
+ * runs out. */
+int lpvo_linear(int dtype, const void* X, int64_t ldx, int64_t M,
+                const void* W, int64_t ldw, int64_t N, int64_t K,
+                int b_r, int b_c, const uint8_t* mask, const void* bias,
+                int gelu, double* Y, int64_t ldy, int nthreads);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

@@ -1,0 +1,331 @@
+"""Pins of the float64 oracle against facts fixed outside it.
+
+Each ``pin_*`` takes an oracle binding (``oracle.Oracle``) and raises
+AssertionError when the oracle disagrees with what the paper, the mathematics
+or an independent library routine fixes.  ``test_oracle_pins.py`` runs them on
+the real oracle; ``test_oracle_mutants.py`` runs them on copies of the oracle
+with planted mistakes and requires every mistake to be caught.
+
+Independent references used here: the hand-worked fixture under ``golden/``,
+the standard normal table, ``scipy.sparse.bsr_matrix`` (BSR arrays),
+``numpy.matmul`` / ``numpy.kron`` (dense products, mask expansion), integer
+arithmetic in int64, torch's CPU bf16 conversion and numpy's float16.
+"""
+import json
+import math
+import os
+
+import numpy as np
+
+import workloads as wl
+
+GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden")
+
+
+def _golden(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return json.load(f)
+
+
+def _expand(mask, b_r, b_c):
+    return np.kron(np.asarray(mask, np.float64), np.ones((b_r, b_c))) != 0
+
+
+def _pruned_f64(W, dtype, mask, b_r, b_c):
+    """Pruned weight in float64 built with numpy (select, not multiply)."""
+    return np.where(_expand(mask, b_r, b_c), wl.to_f32(W, dtype).astype(np.float64), 0.0)
+
+
+def _rand_case(seed, N, K, b_r, b_c, dtype, M=None, p_keep=0.5):
+    g = np.random.default_rng(seed)
+    W = wl.quantize(g.normal(0, 1, (N, K)).astype(np.float32), dtype)
+    mask = (g.random((N // b_r, K // b_c)) < p_keep).astype(np.uint8)
+    bias = wl.quantize(g.normal(0, 1, N).astype(np.float32), dtype)
+    X = wl.quantize(g.normal(0, 1, (M or 8, K)).astype(np.float32), dtype)
+    return X, W, mask, bias
+
+
+# ---------------------------------------------------------------- decoders
+
+def pin_decode_bf16_vs_torch(orc):
+    """Every bf16 bit pattern decodes to torch's own bf16 -> float64 value."""
+    import torch
+    bits = np.arange(1 << 16, dtype=np.uint16)
+    got = orc.decode(bits, "bf16")
+    ref = torch.from_numpy(bits.view(np.int16).copy()).view(torch.bfloat16).to(torch.float64).numpy()
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    # signed zeros survive
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def pin_decode_f16_vs_numpy(orc):
+    """Every binary16 bit pattern decodes to numpy's float16 -> float64 value."""
+    bits = np.arange(1 << 16, dtype=np.uint16)
+    h = bits.view(np.float16)
+    got = orc.decode(h, "f16")
+    ref = h.astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(got[~nan]), np.signbit(ref[~nan]))
+
+
+def pin_decode_f32(orc):
+    g = np.random.default_rng(7)
+    u = g.integers(0, 1 << 32, size=20000, dtype=np.uint64).astype(np.uint32)
+    f = np.concatenate([u.view(np.float32), np.array([0.0, -0.0, np.inf, -np.inf, 1e-45, -3.4e38],
+                                                     np.float32)])
+    got = orc.decode(f, "f32")
+    with np.errstate(invalid="ignore"):
+        ref = f.astype(np.float64)
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(got), nan)
+    assert np.array_equal(got[~nan], ref[~nan])
+
+
+# ---------------------------------------------------------------- GELU
+
+def pin_gelu_normal_table(orc):
+    """GELU(v) = v * Phi(v) at the standard normal table's points, the odd
+    part identity GELU(v) - GELU(-v) = v, and its limits."""
+    from scipy.special import erf
+    for p in _golden("gelu_normal_cdf.json")["points"]:
+        v = p["v"]
+        assert math.isclose(orc.gelu(v), v * p["Phi"], rel_tol=1e-15, abs_tol=1e-300)
+    for v in np.linspace(-6, 6, 97):
+        assert math.isclose(orc.gelu(v) - orc.gelu(-v), v, rel_tol=1e-13, abs_tol=1e-15)
+        ref = 0.5 * v * (1.0 + erf(v / math.sqrt(2.0)))
+        assert math.isclose(orc.gelu(v), ref, rel_tol=1e-14, abs_tol=1e-300)
+    assert orc.gelu(0.0) == 0.0
+    assert orc.gelu(12.0) == 12.0
+    assert orc.gelu(-12.0) == 0.0 or abs(orc.gelu(-12.0)) < 1e-30
+
+
+# ---------------------------------------------------------------- pack
+
+def pin_hand_worked(orc):
+    """The worked 4x4 example with 2x2 blocks (Sec. 3.1 / Sec. 3.4 fixture)."""
+    g = _golden("hand_worked_4x4_2x2.json")
+    W = np.array(g["W"], np.float32)
+    mask = np.array(g["mask"], np.uint8)
+    b_r, b_c = g["b_r"], g["b_c"]
+    assert int(mask.sum()) == g["kept_blocks"] == math.ceil((1 - g["alpha"]) * mask.size)
+    rp, ci, vals = orc.pack(W, "f32", b_r, b_c, mask)
+    assert rp.tolist() == g["row_ptr"]
+    assert ci.tolist() == g["col_idx"]
+    assert vals.tolist() == g["values"]
+    assert orc.unpack(rp, ci, vals, "f32", 4, 4, b_r, b_c).tolist() == g["W_pruned"]
+    X = np.array(g["X"], np.float32)
+    bias = np.array(g["bias"], np.float32)
+    Y = orc.linear(X, W, "f32", b_r, b_c, mask, bias, nthreads=1)
+    assert Y.tolist() == g["Y"]
+
+
+PACK_SHAPES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (32, 64), (64, 64))
+
+
+def pin_pack_vs_scipy(orc):
+    """row_ptr / col_idx / values equal scipy.sparse.bsr_matrix's indptr /
+    indices / data of the pruned weight (no kept block is all zero here)."""
+    import scipy.sparse as sp
+    for i, (b_r, b_c) in enumerate(PACK_SHAPES):
+        for dtype in ("f32", "f16", "bf16"):
+            N, K = 2 * 64, 3 * 64
+            g = np.random.default_rng(100 + i)
+            W = wl.quantize((g.normal(0, 1, (N, K)) + 0.01).astype(np.float32), dtype)
+            Wf = wl.to_f32(W, dtype)
+            assert np.all(Wf != 0)
+            mask = (g.random((N // b_r, K // b_c)) < 0.4).astype(np.uint8)
+            mask[0, :] = 0  # an empty block-row
+            mask[-1, :] = 1  # a full one
+            rp, ci, vals = orc.pack(W, dtype, b_r, b_c, mask)
+            ref = sp.bsr_matrix(np.where(_expand(mask, b_r, b_c), Wf, 0.0).astype(np.float32),
+                                blocksize=(b_r, b_c))
+            ref.sort_indices()
+            assert np.array_equal(rp, ref.indptr)
+            assert np.array_equal(ci, ref.indices)
+            got = wl.to_f32(vals, dtype)
+            assert got.shape == ref.data.shape
+            assert np.array_equal(got, ref.data)
+            assert len(ci) == int(mask.sum())
+
+
+def pin_pack_roundtrip(orc):
+    """unpack(pack(W, mask)) is the selected weight bit for bit, dropped
+    blocks hold +0.0 even where W held NaN or Inf, and pack(unpack(P)) == P."""
+    for i, (b_r, b_c) in enumerate(PACK_SHAPES):
+        for dtype in ("f32", "f16", "bf16"):
+            N, K = 128, 128
+            g = np.random.default_rng(200 + i)
+            W = wl.quantize(g.normal(0, 1, (N, K)).astype(np.float32), dtype)
+            mask = (g.random((N // b_r, K // b_c)) < 0.5).astype(np.uint8)
+            exp = _expand(mask, b_r, b_c)
+            Wbad = W.copy()
+            bad = wl.quantize(np.array([np.nan, np.inf], np.float32), dtype)
+            Wbad[~exp] = bad[0]
+            Wbad[~exp & (np.arange(K)[None, :] % 2 == 0)] = bad[1]
+            rp, ci, vals = orc.pack(Wbad, dtype, b_r, b_c, mask)
+            Wu = orc.unpack(rp, ci, vals, dtype, N, K, b_r, b_c)
+            bits = lambda a: a.view(np.uint32 if a.dtype == np.float32 else np.uint16)
+            assert np.array_equal(bits(Wu)[exp], bits(W)[exp])
+            assert np.all(bits(Wu)[~exp] == 0)
+            rp2, ci2, vals2 = orc.pack(Wu, dtype, b_r, b_c, mask)
+            assert np.array_equal(rp, rp2) and np.array_equal(ci, ci2)
+            assert np.array_equal(bits(vals), bits(vals2))
+
+
+# ---------------------------------------------------------------- contraction
+
+def pin_identity_recovers_weight(orc):
+    """X = I_K gives Y = W~^T + b exactly: row m of Y is column m of the
+    pruned weight.  N != K, so a transposed operand cannot pass."""
+    for dtype, (b_r, b_c) in (("bf16", (32, 16)), ("f32", (16, 32)), ("f16", (64, 32))):
+        N, K = 192, 128
+        _, W, mask, bias = _rand_case(11, N, K, b_r, b_c, dtype)
+        X = wl.quantize(np.eye(K, dtype=np.float32), dtype)
+        Y = orc.linear(X, W, dtype, b_r, b_c, mask, bias, nthreads=3)
+        Wp = _pruned_f64(W, dtype, mask, b_r, b_c)
+        b = wl.to_f32(bias, dtype).astype(np.float64)
+        assert np.array_equal(Y, Wp.T + b[None, :])
+
+
+def pin_onehot_rows(orc):
+    """A one-hot row e_k of X returns column k of the pruned weight scaled by
+    the hot value (a power of two, so exact)."""
+    dtype, b_r, b_c = "bf16", 16, 16
+    N, K = 64, 96
+    _, W, mask, _ = _rand_case(12, N, K, b_r, b_c, dtype)
+    ks = [0, 15, 16, 47, 95]
+    Xf = np.zeros((len(ks), K), np.float32)
+    for i, k in enumerate(ks):
+        Xf[i, k] = 4.0
+    Y = orc.linear(wl.quantize(Xf, dtype), W, dtype, b_r, b_c, mask, None, nthreads=1)
+    Wp = _pruned_f64(W, dtype, mask, b_r, b_c)
+    for i, k in enumerate(ks):
+        assert np.array_equal(Y[i], 4.0 * Wp[:, k])
+
+
+def pin_all_kept_is_dense(orc):
+    """With every block kept the layer is the dense product: numpy.matmul in
+    float64 agrees to float64 rounding."""
+    for dtype in ("f32", "bf16"):
+        X, W, _, bias = _rand_case(13, 96, 160, 32, 32, dtype, M=37)
+        mask = np.ones((3, 5), np.uint8)
+        Y = orc.linear(X, W, dtype, 32, 32, mask, bias, nthreads=2)
+        ref = (wl.to_f32(X, dtype).astype(np.float64) @ wl.to_f32(W, dtype).astype(np.float64).T
+               + wl.to_f32(bias, dtype).astype(np.float64))
+        assert np.max(np.abs(Y - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
+def pin_none_kept_is_bias(orc):
+    """With no block kept the output is the bias, or GELU(bias), exactly."""
+    from scipy.special import erf
+    X, W, _, bias = _rand_case(14, 64, 64, 16, 16, "bf16", M=9)
+    mask = np.zeros((4, 4), np.uint8)
+    b = wl.to_f32(bias, "bf16").astype(np.float64)
+    Y = orc.linear(X, W, "bf16", 16, 16, mask, bias)
+    assert np.array_equal(Y, np.broadcast_to(b, Y.shape))
+    Yg = orc.linear(X, W, "bf16", 16, 16, mask, bias, gelu=True)
+    ref = 0.5 * b * (1.0 + erf(b / math.sqrt(2.0)))
+    assert np.allclose(Yg, np.broadcast_to(ref, Yg.shape), rtol=1e-14, atol=0)
+    Y0 = orc.linear(X, W, "bf16", 16, 16, mask, None)
+    assert np.all(Y0 == 0.0)
+
+
+def pin_complement_additivity(orc):
+    """Y(mask) + Y(not mask) - b = Y(all kept): every block is counted once."""
+    X, W, mask, bias = _rand_case(15, 128, 96, 32, 16, "f16", M=21)
+    full = np.ones_like(mask)
+    b = wl.to_f32(bias, "f16").astype(np.float64)
+    Ya = orc.linear(X, W, "f16", 32, 16, mask, bias)
+    Yb = orc.linear(X, W, "f16", 32, 16, 1 - mask, bias)
+    Yf = orc.linear(X, W, "f16", 32, 16, full, bias)
+    assert np.max(np.abs(Ya + Yb - b - Yf)) <= 1e-12 * np.max(np.abs(Yf))
+
+
+def pin_bruteforce_tiny(orc):
+    """Tiny shapes of every block shape: direct summation over the kept
+    blocks only, in pure Python, walking the mask block by block."""
+    for i, (b_r, b_c) in enumerate(PACK_SHAPES):
+        N, K, M = 2 * b_r, 2 * b_c, 3
+        X, W, mask, bias = _rand_case(300 + i, N, K, b_r, b_c, "bf16", M=M, p_keep=0.6)
+        Xf = wl.to_f32(X, "bf16").astype(np.float64).tolist()
+        Wf = wl.to_f32(W, "bf16").astype(np.float64).tolist()
+        bf = wl.to_f32(bias, "bf16").astype(np.float64).tolist()
+        ref = [[bf[n] for n in range(N)] for _ in range(M)]
+        for r in range(N // b_r):
+            for c in range(K // b_c):
+                if not mask[r][c]:
+                    continue
+                for m in range(M):
+                    for i2 in range(b_r):
+                        s = 0.0
+                        for j2 in range(b_c):
+                            s += Xf[m][c * b_c + j2] * Wf[r * b_r + i2][c * b_c + j2]
+                        ref[m][r * b_r + i2] += s
+        Y = orc.linear(X, W, "bf16", b_r, b_c, mask, bias, nthreads=1)
+        ref = np.array(ref)
+        assert np.max(np.abs(Y - ref)) <= 1e-12 * max(1.0, np.max(np.abs(ref)))
+
+
+def pin_exact_integers(orc):
+    """Small-integer inputs: the product is exact in float64 and must equal
+    the int64 product of the selected weight."""
+    g = np.random.default_rng(16)
+    for dtype, (b_r, b_c) in (("bf16", (32, 32)), ("f16", (16, 64)), ("f32", (64, 16))):
+        M, N, K = 33, 128, 192
+        Xi = g.integers(-2, 3, size=(M, K))
+        Wi = g.integers(-2, 3, size=(N, K))
+        bi = g.integers(-4, 5, size=N)
+        mask = (g.random((N // b_r, K // b_c)) < 0.5).astype(np.uint8)
+        ref = Xi @ np.where(_expand(mask, b_r, b_c), Wi, 0).T + bi
+        Y = orc.linear(wl.quantize(Xi, dtype), wl.quantize(Wi, dtype), dtype, b_r, b_c, mask,
+                       wl.quantize(bi, dtype), nthreads=4)
+        assert np.array_equal(Y, ref.astype(np.float64))
+
+
+def pin_nonfinite_in_dropped_blocks(orc):
+    """NaN / Inf stored in dropped blocks never reaches Y; a NaN in a kept
+    block does (the oracle does not hide bad kept weights)."""
+    X, W, mask, bias = _rand_case(17, 64, 64, 16, 16, "bf16", M=5)
+    mask[1, 2] = 0
+    mask[0, 0] = 1
+    clean = orc.linear(X, W, "bf16", 16, 16, mask, bias)
+    W2 = W.copy()
+    exp = _expand(mask, 16, 16)
+    W2[~exp] = wl.quantize(np.array([np.nan], np.float32), "bf16")[0]
+    W2[16:32, 32:48] = wl.quantize(np.array([np.inf], np.float32), "bf16")[0]
+    assert np.array_equal(orc.linear(X, W2, "bf16", 16, 16, mask, bias), clean)
+    W3 = W.copy()
+    W3[0, 0] = wl.quantize(np.array([np.nan], np.float32), "bf16")[0]
+    Y3 = orc.linear(X, W3, "bf16", 16, 16, mask, bias)
+    assert np.all(np.isnan(Y3[:, 0]))
+
+
+def pin_thread_invariance(orc):
+    X, W, mask, bias = _rand_case(18, 96, 64, 32, 32, "f32", M=50)
+    Y1 = orc.linear(X, W, "f32", 32, 32, mask, bias, gelu=True, nthreads=1)
+    Y7 = orc.linear(X, W, "f32", 32, 32, mask, bias, gelu=True, nthreads=7)
+    assert np.array_equal(Y1, Y7)
+
+
+def pin_rejects_bad_grids(orc):
+    """Block sizes that do not divide the weight are rejected (the score grid
+    has H/B_h x W/B_w entries, Sec. 3.1)."""
+    W = np.zeros((48, 64), np.float32)
+    for b_r, b_c in ((32, 32), (16, 48), (0, 16)):
+        try:
+            orc.pack(W, "f32", b_r, b_c, np.ones((max(1, 48 // max(b_r, 1)), 1), np.uint8))
+        except ValueError:
+            continue
+        raise AssertionError("block %dx%d accepted for a 48x64 weight" % (b_r, b_c))
+    m = np.ones(64, np.uint8)
+    assert orc.lib.lpvo_pack(0, W.ctypes.data, 64, 48, 64, 32, 32, m.ctypes.data,
+                             None, None, None) == -1
+    assert orc.lib.lpvo_pack(0, W.ctypes.data, 64, 48, 64, 16, 16, m.ctypes.data,
+                             None, None, None) == 12
+
+
+ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]
