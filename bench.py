@@ -1,0 +1,222 @@
+"""Benchmark of the block-sparse linear layer on one MI355X.
+
+Workload (default): DeiT-B fc1 at batch 256 -- X bf16 [50432 x 768] ~ N(0,1),
+W bf16 [3072 x 768] ~ N(0, 0.02), bias, 32x32 blocks, 50% of the blocks kept
+uniformly at random (exactly 1152 of 2304), no GELU.
+
+A step is one lpv_bsr_linear call over the whole batch (X staging, kept-block
+contraction, epilogue); the weight is packed once before timing (weights are
+static at inference) and the pack is timed on its own.  The dense path
+(lpv_dense_linear, same shape, same epilogue) is timed the same way for the
+speed-up.  Prints ONE JSON line on stdout; details go to stderr.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--gelu]
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16/fp16 matrix-core peak (published)
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bsr_linear_fc1_hbm_traffic.json")
+KERNEL_SOURCES = ("paper_2407_02068_amd/csrc/linear.hip", "paper_2407_02068_amd/csrc/lpv_device.h",
+                  "paper_2407_02068_amd/csrc/lpv_internal.h")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch of the block-sparse kernel from the committed
+    rocprofv3 counter summary, if it was taken on the current kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel_source_sha256_16") != kernel_source_hash():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def algorithmic_bytes(M, N, K, nnzb, b_r, b_c, kused_cols, es=2):
+    """X (used columns only) + Y + kept W + bias + BSR indices, each once."""
+    return es * (M * kused_cols + M * N + nnzb * b_r * b_c + N) + 4 * (N // b_r + 1 + nnzb)
+
+
+def time_launches(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        starts[i].record()
+        fn()
+        ends[i].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
+    return wall, ms
+
+
+def pct(ms, q):
+    return ms[min(len(ms) - 1, int(q * (len(ms) - 1) + 0.5))]
+
+
+def cpu_baseline(w, target_s=12.0):
+    """The float64 oracle on the host cores, on a bounded sample of token
+    rows of the same workload; reported as effective TFLOP/s on kept blocks."""
+    import numpy as np
+    import oracle
+    nt = oracle.default_threads()
+    rows = 64
+    t = 0.0
+    while True:
+        X = w.X[:rows]
+        t0 = time.perf_counter()
+        oracle.linear(X, w.W, w.dtype, w.b_r, w.b_c, w.mask, w.bias, gelu=w.gelu, nthreads=nt)
+        t = time.perf_counter() - t0
+        if t >= target_s / 4 or rows >= w.M:
+            break
+        rows = min(w.M, int(rows * max(2.0, target_s / 4 / max(t, 1e-3))))
+    flops = w.kept_flops(rows)
+    return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": nt, "kind": "oracle",
+            "sample": "first %d of %d token rows of the same workload (float64 mask expansion + "
+                      "triple loop), %.1f s" % (rows, w.M, t)}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
+    ap.add_argument("--dtype", default="bf16", choices=["bf16", "f16"])
+    ap.add_argument("--block", type=int, default=32)
+    ap.add_argument("--sparsity", type=int, default=50)
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the block-sparse layer shards over tokens with no "
+              "exchange, so a multi-GPU run is N independent copies; run with --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_2407_02068_amd import lpv
+
+    lpv.lib()
+    torch.cuda.set_device(0)
+    w = wl.b_fc1(block=args.block, sparsity=args.sparsity, dtype=args.dtype, gelu=args.gelu)
+    M, N, K = w.M, w.N, w.K
+    tt = torch.bfloat16 if w.dtype == "bf16" else torch.float16
+
+    def to_dev(a):
+        a = np.ascontiguousarray(a)
+        if w.dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    X, W, b = to_dev(w.X), to_dev(w.W), to_dev(w.bias)
+    mask = torch.from_numpy(w.mask).cuda()
+    Y = torch.empty((M, N), dtype=tt, device="cuda")
+    Yd = torch.empty((M, N), dtype=tt, device="cuda")
+    epi = "gelu" if w.gelu else None
+    log("workload %s: M=%d N=%d K=%d nnzb=%d" % (w.name, M, N, K, w.nnzb))
+
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    h = lpv.bsr_pack(W, mask, w.b_r, w.b_c)
+    pack_ms = (time.perf_counter() - t0) * 1e3
+
+    sparse = lambda: lpv.bsr_linear(h, X, b, Y, epi=epi)
+    dense = lambda: lpv.dense_linear(W, X, b, Yd, epi=epi)
+    wall, ms = time_launches(sparse, args.steps, args.warmup)
+    dwall, dms = time_launches(dense, args.steps, args.warmup)
+    # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
+    bl = lambda: torch.addmm(b, X, W.t())
+    _, bms = time_launches(bl, max(5, args.steps // 2), 3)
+
+    kept_flops = w.kept_flops()
+    ms_step = wall / args.steps * 1e3
+    value = kept_flops / (wall / args.steps) / 1e12
+    ev_avg = sum(ms) / len(ms)
+    achieved = kept_flops / (ev_avg * 1e-3) / 1e12
+    kused = int((w.mask.sum(axis=0) > 0).sum()) * w.b_c
+    alg_bytes = algorithmic_bytes(M, N, K, w.nnzb, w.b_r, w.b_c, kused)
+    hbm_gbs = alg_bytes / (ev_avg * 1e-3) / 1e9
+    traffic = measured_traffic()
+    dense_avg = sum(dms) / len(dms)
+    log("bsr_linear: median %.1f us (p10 %.1f, p90 %.1f), %.0f TFLOP/s effective, %.0f GB/s alg."
+        % (pct(ms, .5) * 1e3, pct(ms, .1) * 1e3, pct(ms, .9) * 1e3, achieved, hbm_gbs))
+    log("dense_linear: median %.1f us, %.0f TFLOP/s; hipBLASLt addmm median %.1f us"
+        % (pct(dms, .5) * 1e3, w.dense_flops() / (dense_avg * 1e-3) / 1e12, pct(bms, .5) * 1e3))
+    log("pack: %.2f ms (one-time)" % pack_ms)
+
+    out = {
+        "metric": "effective TFLOP/s + speedup vs dense, DeiT-B fc1 at 50% block sparsity",
+        "value": round(value, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": "DeiT-B fc1 batch 256: X [%d x %d] -> %d, %dx%d blocks, %d%% block "
+                               "sparsity (uniform, exact count), %s, bias%s"
+                               % (M, K, N, w.b_r, w.b_c, args.sparsity, w.dtype,
+                                  " + GELU" if w.gelu else ", no GELU"),
+                   "M": M, "N": N, "K": K, "block": [w.b_r, w.b_c], "sparsity_pct": args.sparsity,
+                   "nnzb": w.nnzb, "kept_gflop": round(kept_flops / 1e9, 2)},
+        "speedup_vs_dense": round(dense_avg / ev_avg, 3),
+        "dense_ms": round(dense_avg, 5),
+        "bsr_ms_median": round(pct(ms, .5), 5),
+        "bsr_ms_p10": round(pct(ms, .1), 5),
+        "bsr_ms_p90": round(pct(ms, .9), 5),
+        "hipblaslt_addmm_ms": round(pct(bms, .5), 5),
+        "pack_ms": round(pack_ms, 3),
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": traffic,
+                     "kernel": "k_linear16 (lpv_bsr_linear)",
+                     "hbm_alg_bytes": alg_bytes, "hbm_achieved_GBs": round(hbm_gbs, 1),
+                     "hbm_peak_GBs": PEAK_HBM_GBS, "hbm_frac": round(hbm_gbs / PEAK_HBM_GBS, 4)},
+    }
+    if not args.no_cpu:
+        log("timing the CPU oracle on a sample ...")
+        out["cpu_baseline"] = cpu_baseline(w)
+    else:
+        out["cpu_baseline"] = None
+    h.close()
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

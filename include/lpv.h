@@ -1,0 +1,187 @@
+/*
+ * lpv.h -- C ABI of liblpv, a block-sparse linear layer for AMD MI355X (gfx950).
+ *
+ * The layer is the one that block-structured pruning of vision transformers
+ * (LPViT, arXiv 2407.02068) makes cheaper:
+ *
+ *     Y = g(X * W~^T + b)
+ *
+ * X is the dense token-by-channel activation (M tokens x K input features), W is
+ * a linear weight in the nn.Linear layout (N output features x K input
+ * features), b the bias and g the identity or GELU.  W~ is W with whole blocks
+ * removed: the weight is cut into a grid of b_r x b_c blocks, a binary block
+ * mask keeps or drops each block, and W~[n][k] = W[n][k] when the block
+ * (n / b_r, k / b_c) is kept and 0 otherwise (the paper's masked weight, Sec.
+ * 3.1).  The work of the layer is proportional to the number of kept blocks
+ * times the number of token tiles (the per-matmul cost model of Sec. 3.4).
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Pointers named as device pointers are HIP device memory of the current
+ *   device; the caller owns them.  The library keeps no caller pointer after a
+ *   call returns.
+ * - Matrices are row-major with a leading dimension in ELEMENTS (ldx, ldw,
+ *   ldy).  Device pointers must be 16-byte aligned and ld * element size must be
+ *   a multiple of 16 bytes; otherwise LPV_ERR_INVALID_ARG.
+ * - X, W, bias and Y share one element type (lpv_dtype).  Arithmetic inside
+ *   the kernels is float32 (bf16/fp16 inputs go to the matrix cores with float32
+ *   accumulation); the result is rounded once, to nearest even, to the element
+ *   type.
+ * - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *   enqueues work on it and returns, except lpv_bsr_pack, which waits once for
+ *   its own work (see there).
+ * - Every argument is checked before any HIP call; a bad argument returns a
+ *   negative lpv_status and changes nothing.  lpv_last_error() then gives a
+ *   message for the calling thread.  No exception crosses the ABI.
+ * - Block sides b_r and b_c are each 16, 32 or 64 (the block shapes of the
+ *   paper's experiments, Tables 2 and 4); they must divide N and K exactly (the
+ *   block-score grid of Sec. 3.1 has N/b_r x K/b_c entries), else
+ *   LPV_ERR_SHAPE.  Non-finite values in X are outside the contract.
+ */
+#ifndef LPV_H
+#define LPV_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    LPV_OK = 0,
+    LPV_ERR_INVALID_ARG = -1, /* null pointer, bad leading dimension, misalignment */
+    LPV_ERR_SHAPE = -2,       /* sizes out of range or not divisible by the block */
+    LPV_ERR_DTYPE = -3,       /* unknown element type */
+    LPV_ERR_BLOCK = -4,       /* block side not in {16, 32, 64} */
+    LPV_ERR_ALIAS = -5,       /* X and Y overlap */
+    LPV_ERR_ALLOC = -6,       /* device or host allocation failed */
+    LPV_ERR_HIP = -7          /* a HIP runtime call failed; see lpv_last_error() */
+} lpv_status;
+
+typedef enum { LPV_F32 = 0, LPV_F16 = 1, LPV_BF16 = 2 } lpv_dtype;
+
+typedef enum { LPV_EPI_NONE = 0, LPV_EPI_GELU = 1 } lpv_epilogue;
+
+/* A packed block-sparse weight.  Opaque; owns its device buffers; immutable
+ * after lpv_bsr_pack returns, so calls on different streams may share it. */
+typedef struct lpv_bsr lpv_bsr;
+
+typedef struct {
+    int64_t N, K;         /* weight shape: output x input features */
+    int32_t b_r, b_c;     /* block shape */
+    int32_t R, C;         /* block grid: N / b_r x K / b_c */
+    int64_t nnzb;         /* kept blocks */
+    int32_t dtype;        /* lpv_dtype */
+    int32_t device;       /* HIP device the buffers live on */
+    /* tile schedule (see lpv_bsr_schedule_export) */
+    int32_t tile_rows;    /* output rows per schedule tile (32) */
+    int32_t tile_cols;    /* reduction columns per schedule tile (32) */
+    int32_t group_tiles;  /* tile rows per group */
+    int32_t n_groups;     /* groups of tile rows */
+    int64_t n_steps;      /* (group, tile column) pairs with work */
+    int64_t n_tiles;      /* kept (tile row, tile column) pairs */
+} lpv_bsr_info;
+
+/*
+ * lpv_bsr_pack -- mask -> BSR (block compressed sparse row), on the GPU.
+ *
+ * Paper: the pruned weight W~ = W (.) M over b_r x b_c blocks (Sec. 3.1); the
+ * kept-block count is the block count of the cost model (Sec. 3.4).
+ *
+ * W     device, N x K, row stride ldw >= K, element type dt.
+ * mask  device, uint8, R x C = (N / b_r) x (K / b_c), row-major; nonzero keeps
+ *       the block.
+ * out   host; receives a new handle (NULL on failure).
+ *
+ * The handle holds the canonical BSR arrays: row_ptr[R + 1] (row_ptr[0] = 0,
+ * row_ptr[r + 1] - row_ptr[r] = kept blocks of block-row r), col_idx[nnzb]
+ * (ascending within a block-row) and values[nnzb][b_r][b_c] (raw element bits
+ * of each kept block, row-major), plus the tile schedule and an internal copy
+ * of the kept values in matrix-core operand order.  Dropped blocks are never
+ * read by lpv_bsr_linear, so NaN or Inf in them cannot reach Y.
+ *
+ * Allocates device memory (freed by lpv_bsr_destroy) and waits once on
+ * `stream` to learn the kept count.  W and mask may be freed afterwards.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, BLOCK, ALLOC, HIP.
+ */
+lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                        int32_t b_r, int32_t b_c, const uint8_t* mask, void* stream,
+                        lpv_bsr** out);
+
+/* Shape, kept count and schedule sizes of a handle (host struct). */
+lpv_status lpv_bsr_info_get(const lpv_bsr* h, lpv_bsr_info* out);
+
+/*
+ * lpv_bsr_export -- copy the canonical BSR arrays (described at lpv_bsr_pack)
+ * into caller device buffers: row_ptr int32[R + 1], col_idx int32[nnzb],
+ * values [nnzb][b_r][b_c] of the handle's element type.  Any of the three may
+ * be NULL to skip it.  Asynchronous on `stream`.
+ */
+lpv_status lpv_bsr_export(const lpv_bsr* h, int32_t* row_ptr, int32_t* col_idx, void* values,
+                          void* stream);
+
+/*
+ * lpv_bsr_schedule_export -- copy the tile schedule into caller device buffers
+ * (each may be NULL):
+ *   group_order int32[n_groups]      groups in launch order (most work first);
+ *   step_ptr    int32[n_groups + 1]  steps of group g are [step_ptr[g], step_ptr[g+1]);
+ *   step_col    int32[n_steps]       tile column of each step, ascending per group;
+ *   step_bits   int32[n_steps]       bit j set when tile row g*group_tiles + j keeps
+ *                                    tile (row, step_col);
+ *   step_tile   int32[n_steps]       index of the step's first kept tile in the
+ *                                    operand-order value stream (prefix sum of
+ *                                    popcount(step_bits)).
+ * A tile is tile_rows x tile_cols elements of W; it is kept when any element of
+ * it lies in a kept block.  Asynchronous on `stream`.
+ */
+lpv_status lpv_bsr_schedule_export(const lpv_bsr* h, int32_t* group_order, int32_t* step_ptr,
+                                   int32_t* step_col, int32_t* step_bits, int32_t* step_tile,
+                                   void* stream);
+
+/*
+ * lpv_bsr_unpack -- the pruned dense weight W~ (N x K, row stride ldw >= K) into
+ * a caller device buffer; dropped blocks become +0.0.  Asynchronous.
+ */
+lpv_status lpv_bsr_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, void* stream);
+
+/*
+ * lpv_bsr_linear -- Y = g(X * W~^T + b), the block-sparse hot path.
+ *
+ * X     device, M x K, row stride ldx >= K.
+ * bias  device, N elements, or NULL for no bias.
+ * Y     device, M x N, row stride ldy >= N; must not overlap X.
+ * epi   LPV_EPI_NONE or LPV_EPI_GELU (exact-erf GELU after the bias).
+ *
+ * Each token tile times each group of output tile rows walks only the kept
+ * tiles of its rows, on the matrix cores for bf16/fp16.  M = 0 is a no-op.
+ * One kernel launch, no allocation, no host synchronisation.
+ * Errors: INVALID_ARG, SHAPE, ALIAS, HIP.
+ */
+lpv_status lpv_bsr_linear(const lpv_bsr* h, const void* X, int64_t ldx, int64_t M,
+                          const void* bias, void* Y, int64_t ldy, lpv_epilogue epi,
+                          void* stream);
+
+/*
+ * lpv_dense_linear -- Y = g(X * W^T + b) with a dense W (N x K, row stride ldw),
+ * through the library's own matrix-core kernel: the reference point for the
+ * speed-up of the block-sparse path.  Same conventions as lpv_bsr_linear;
+ * N and K must be multiples of 16.
+ */
+lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                            const void* X, int64_t ldx, int64_t M, const void* bias, void* Y,
+                            int64_t ldy, lpv_epilogue epi, void* stream);
+
+/* Release a handle and its device buffers.  NULL-safe.  The caller must make
+ * sure no enqueued work still uses it. */
+void lpv_bsr_destroy(lpv_bsr* h);
+
+/* Static name of a status code. */
+const char* lpv_status_str(lpv_status s);
+
+/* Detail of the calling thread's last failed call ("" if none). */
+const char* lpv_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* LPV_H */

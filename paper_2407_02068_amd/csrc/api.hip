@@ -1,0 +1,376 @@
+// api.hip -- the C ABI of liblpv (include/lpv.h): argument checks, the packed
+// weight handle, device memory and kernel dispatch.
+//
+// Every check runs before the first HIP call, so a rejected call touches no
+// device state (and the checks can be exercised on a machine without a GPU).
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <new>
+
+#include "lpv_internal.h"
+
+namespace {
+
+thread_local char g_err[512];
+
+lpv_status fail(lpv_status s, const char* fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+lpv_status hip_fail(hipError_t e, const char* what)
+{
+    return fail(LPV_ERR_HIP, "%s: %s (%d)", what, hipGetErrorString(e), (int)e);
+}
+
+int elem_size(int dt)
+{
+    switch (dt) {
+    case LPV_F32: return 4;
+    case LPV_F16: return 2;
+    case LPV_BF16: return 2;
+    default: return 0;
+    }
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+constexpr int64_t MAX_DIM = 65536;  // N and K (schedule tables are sized for it)
+constexpr int64_t MAX_M = (int64_t)1 << 31;
+
+// Device allocations fail on purpose when LPV_FAULT_INJECT=alloc (tests of
+// the error path).
+bool inject_alloc_failure()
+{
+    const char* v = getenv("LPV_FAULT_INJECT");
+    return v && strcmp(v, "alloc") == 0;
+}
+
+hipError_t dmalloc(void** p, size_t bytes)
+{
+    *p = nullptr;
+    if (inject_alloc_failure())
+        return hipErrorOutOfMemory;
+    if (bytes == 0)
+        return hipSuccess;
+    return hipMalloc(p, bytes);
+}
+
+lpv_status check_block(int32_t b)
+{
+    return (b == 16 || b == 32 || b == 64) ? LPV_OK : LPV_ERR_BLOCK;
+}
+
+// Shared checks of the linear calls: X (M x K, ldx), Y (M x N, ldy), bias.
+lpv_status check_linear(int es, int64_t N, int64_t K, const void* X, int64_t ldx, int64_t M,
+                        const void* bias, const void* Y, int64_t ldy, int epi)
+{
+    if (M < 0 || M >= MAX_M)
+        return fail(LPV_ERR_SHAPE, "M = %lld is out of range [0, 2^31)", (long long)M);
+    if (epi != LPV_EPI_NONE && epi != LPV_EPI_GELU)
+        return fail(LPV_ERR_INVALID_ARG, "unknown epilogue %d", epi);
+    if (ldx < K)
+        return fail(LPV_ERR_INVALID_ARG, "ldx = %lld < K = %lld", (long long)ldx, (long long)K);
+    if (ldy < N)
+        return fail(LPV_ERR_INVALID_ARG, "ldy = %lld < N = %lld", (long long)ldy, (long long)N);
+    if ((ldx * es) % 16 || (ldy * es) % 16)
+        return fail(LPV_ERR_INVALID_ARG, "ldx and ldy must be multiples of 16 bytes");
+    if (M == 0)
+        return LPV_OK;
+    if (!X || !Y)
+        return fail(LPV_ERR_INVALID_ARG, "X and Y must not be NULL when M > 0");
+    if (!aligned16(X) || !aligned16(Y) || (bias && !aligned16(bias)))
+        return fail(LPV_ERR_INVALID_ARG, "X, Y and bias must be 16-byte aligned");
+    const uintptr_t x0 = (uintptr_t)X, x1 = x0 + (uintptr_t)(((M - 1) * ldx + K) * es);
+    const uintptr_t y0 = (uintptr_t)Y, y1 = y0 + (uintptr_t)(((M - 1) * ldy + N) * es);
+    if (x0 < y1 && y0 < x1)
+        return fail(LPV_ERR_ALIAS, "X and Y overlap");
+    return LPV_OK;
+}
+
+void free_handle(lpv_bsr* h)
+{
+    if (!h)
+        return;
+    void* bufs[] = {h->meta, h->col_idx, h->values, h->step_col, h->step_bits, h->step_tile,
+                    h->stream_vals};
+    for (void* p : bufs)
+        if (p)
+            (void)hipFree(p);
+    delete h;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lpv_status_str(lpv_status s)
+{
+    switch (s) {
+    case LPV_OK: return "LPV_OK";
+    case LPV_ERR_INVALID_ARG: return "LPV_ERR_INVALID_ARG";
+    case LPV_ERR_SHAPE: return "LPV_ERR_SHAPE";
+    case LPV_ERR_DTYPE: return "LPV_ERR_DTYPE";
+    case LPV_ERR_BLOCK: return "LPV_ERR_BLOCK";
+    case LPV_ERR_ALIAS: return "LPV_ERR_ALIAS";
+    case LPV_ERR_ALLOC: return "LPV_ERR_ALLOC";
+    case LPV_ERR_HIP: return "LPV_ERR_HIP";
+    default: return "LPV_ERR_UNKNOWN";
+    }
+}
+
+const char* lpv_last_error(void) { return g_err; }
+
+lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                        int32_t b_r, int32_t b_c, const uint8_t* mask, void* stream,
+                        lpv_bsr** out)
+{
+    g_err[0] = 0;
+    if (!out)
+        return fail(LPV_ERR_INVALID_ARG, "out must not be NULL");
+    *out = nullptr;
+    const int es = elem_size(dt);
+    if (!es)
+        return fail(LPV_ERR_DTYPE, "unknown element type %d", (int)dt);
+    if (check_block(b_r) || check_block(b_c))
+        return fail(LPV_ERR_BLOCK, "block %dx%d: each side must be 16, 32 or 64", b_r, b_c);
+    if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM)
+        return fail(LPV_ERR_SHAPE, "weight %lldx%lld: each side must be in [1, %lld]",
+                    (long long)N, (long long)K, (long long)MAX_DIM);
+    if (N % b_r || K % b_c)
+        return fail(LPV_ERR_SHAPE, "block %dx%d does not divide weight %lldx%lld", b_r, b_c,
+                    (long long)N, (long long)K);
+    if (!W || !mask)
+        return fail(LPV_ERR_INVALID_ARG, "W and mask must not be NULL");
+    if (ldw < K || (ldw * es) % 16 || !aligned16(W))
+        return fail(LPV_ERR_INVALID_ARG, "W must be 16-byte aligned with ldw >= K and ldw a "
+                                         "multiple of 16 bytes");
+
+    lpv_bsr* h = new (std::nothrow) lpv_bsr();
+    if (!h)
+        return fail(LPV_ERR_ALLOC, "host allocation failed");
+    h->N = N;
+    h->K = K;
+    h->b_r = b_r;
+    h->b_c = b_c;
+    h->R = (int32_t)(N / b_r);
+    h->C = (int32_t)(K / b_c);
+    h->dtype = dt;
+    h->n_tile_rows = (int32_t)((N + lpv::TILE - 1) / lpv::TILE);
+    h->n_tile_cols = (int32_t)((K + lpv::TILE - 1) / lpv::TILE);
+    h->n_groups = (h->n_tile_rows + lpv::GROUP_TILES - 1) / lpv::GROUP_TILES;
+    hipStream_t s = (hipStream_t)stream;
+
+    // one buffer for row_ptr, group_order, step_ptr, group_tile0 and the plan
+    const size_t n_meta = (size_t)(h->R + 1) + 3 * (size_t)(h->n_groups + 1) + 4;
+    void* meta = nullptr;
+    hipError_t e = dmalloc(&meta, n_meta * sizeof(int32_t));
+    if (e != hipSuccess) {
+        free_handle(h);
+        return e == hipErrorOutOfMemory ? fail(LPV_ERR_ALLOC, "device allocation failed")
+                                        : hip_fail(e, "hipMalloc");
+    }
+    h->meta = meta;
+    e = hipGetDevice(&h->device);
+    if (e != hipSuccess) {
+        free_handle(h);
+        return hip_fail(e, "hipGetDevice");
+    }
+    h->row_ptr = (int32_t*)meta;
+    h->group_order = h->row_ptr + (h->R + 1);
+    h->step_ptr = h->group_order + (h->n_groups + 1);
+    h->group_tile0 = h->step_ptr + (h->n_groups + 1);
+    lpv::Plan* plan_d = (lpv::Plan*)(h->group_tile0 + (h->n_groups + 1));
+
+    lpv::PackArgs a = {};
+    a.W = W;
+    a.ldw = ldw;
+    a.N = N;
+    a.K = K;
+    a.es = es;
+    a.b_r = b_r;
+    a.b_c = b_c;
+    a.R = h->R;
+    a.C = h->C;
+    a.mask = mask;
+    a.n_tile_rows = h->n_tile_rows;
+    a.n_tile_cols = h->n_tile_cols;
+    a.n_groups = h->n_groups;
+
+    lpv::Plan plan = {};
+    e = lpv::launch_pack_plan(a, h->row_ptr, h->step_ptr, h->group_tile0, h->group_order, plan_d, s);
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(&plan, plan_d, sizeof plan, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        free_handle(h);
+        return hip_fail(e, "pack plan");
+    }
+    h->nnzb = plan.nnzb;
+    const bool mfma_path = dt != LPV_F32;
+    h->n_steps = mfma_path ? plan.n_steps : 0;
+    h->n_tiles = mfma_path ? plan.n_tiles : 0;
+
+    const size_t blk = (size_t)b_r * b_c * es;
+    e = dmalloc((void**)&h->col_idx, (size_t)h->nnzb * sizeof(int32_t));
+    if (e == hipSuccess)
+        e = dmalloc(&h->values, (size_t)h->nnzb * blk);
+    if (e == hipSuccess && mfma_path) {
+        e = dmalloc((void**)&h->step_col, (size_t)h->n_steps * sizeof(int32_t));
+        if (e == hipSuccess)
+            e = dmalloc((void**)&h->step_bits, (size_t)h->n_steps * sizeof(int32_t));
+        if (e == hipSuccess)
+            e = dmalloc((void**)&h->step_tile, (size_t)h->n_steps * sizeof(int32_t));
+        if (e == hipSuccess)
+            e = dmalloc(&h->stream_vals, (size_t)h->n_tiles * lpv::TILE * lpv::TILE * es);
+    }
+    if (e != hipSuccess) {
+        free_handle(h);
+        return e == hipErrorOutOfMemory ? fail(LPV_ERR_ALLOC, "device allocation failed")
+                                        : hip_fail(e, "hipMalloc");
+    }
+    e = lpv::launch_pack_fill(a, h, s);
+    if (e == hipSuccess)
+        e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        free_handle(h);
+        return hip_fail(e, "pack fill");
+    }
+    *out = h;
+    return LPV_OK;
+}
+
+lpv_status lpv_bsr_info_get(const lpv_bsr* h, lpv_bsr_info* out)
+{
+    if (!h || !out)
+        return fail(LPV_ERR_INVALID_ARG, "handle and out must not be NULL");
+    out->N = h->N;
+    out->K = h->K;
+    out->b_r = h->b_r;
+    out->b_c = h->b_c;
+    out->R = h->R;
+    out->C = h->C;
+    out->nnzb = h->nnzb;
+    out->dtype = h->dtype;
+    out->device = h->device;
+    out->tile_rows = lpv::TILE;
+    out->tile_cols = lpv::TILE;
+    out->group_tiles = lpv::GROUP_TILES;
+    out->n_groups = h->dtype == LPV_F32 ? 0 : h->n_groups;
+    out->n_steps = h->n_steps;
+    out->n_tiles = h->n_tiles;
+    return LPV_OK;
+}
+
+lpv_status lpv_bsr_export(const lpv_bsr* h, int32_t* row_ptr, int32_t* col_idx, void* values,
+                          void* stream)
+{
+    if (!h)
+        return fail(LPV_ERR_INVALID_ARG, "handle must not be NULL");
+    hipStream_t s = (hipStream_t)stream;
+    const size_t blk = (size_t)h->b_r * h->b_c * elem_size(h->dtype);
+    hipError_t e = hipSuccess;
+    if (row_ptr)
+        e = hipMemcpyAsync(row_ptr, h->row_ptr, (size_t)(h->R + 1) * sizeof(int32_t),
+                           hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && col_idx && h->nnzb)
+        e = hipMemcpyAsync(col_idx, h->col_idx, (size_t)h->nnzb * sizeof(int32_t),
+                           hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess && values && h->nnzb)
+        e = hipMemcpyAsync(values, h->values, (size_t)h->nnzb * blk, hipMemcpyDeviceToDevice, s);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "export copy");
+}
+
+lpv_status lpv_bsr_schedule_export(const lpv_bsr* h, int32_t* group_order, int32_t* step_ptr,
+                                   int32_t* step_col, int32_t* step_bits, int32_t* step_tile,
+                                   void* stream)
+{
+    if (!h)
+        return fail(LPV_ERR_INVALID_ARG, "handle must not be NULL");
+    if (h->dtype == LPV_F32)
+        return fail(LPV_ERR_DTYPE, "fp32 handles walk the BSR arrays and carry no tile schedule");
+    hipStream_t s = (hipStream_t)stream;
+    hipError_t e = hipSuccess;
+    const size_t ng = (size_t)h->n_groups, ns = (size_t)h->n_steps;
+    struct {
+        void* dst;
+        const void* src;
+        size_t n;
+    } cp[] = {{group_order, h->group_order, ng},
+              {step_ptr, h->step_ptr, ng + 1},
+              {step_col, h->step_col, ns},
+              {step_bits, h->step_bits, ns},
+              {step_tile, h->step_tile, ns}};
+    for (auto& c : cp)
+        if (e == hipSuccess && c.dst && c.n)
+            e = hipMemcpyAsync(c.dst, c.src, c.n * sizeof(int32_t), hipMemcpyDeviceToDevice, s);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "schedule copy");
+}
+
+lpv_status lpv_bsr_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, void* stream)
+{
+    if (!h)
+        return fail(LPV_ERR_INVALID_ARG, "handle must not be NULL");
+    const int es = elem_size(h->dtype);
+    if (!W_out || ldw < h->K || (ldw * es) % 16 || !aligned16(W_out))
+        return fail(LPV_ERR_INVALID_ARG, "W_out must be 16-byte aligned with ldw >= K and ldw a "
+                                         "multiple of 16 bytes");
+    hipError_t e = lpv::launch_unpack(h, W_out, ldw, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "unpack launch");
+}
+
+lpv_status lpv_bsr_linear(const lpv_bsr* h, const void* X, int64_t ldx, int64_t M,
+                          const void* bias, void* Y, int64_t ldy, lpv_epilogue epi, void* stream)
+{
+    if (!h)
+        return fail(LPV_ERR_INVALID_ARG, "handle must not be NULL");
+    lpv_status st = check_linear(elem_size(h->dtype), h->N, h->K, X, ldx, M, bias, Y, ldy, epi);
+    if (st != LPV_OK || M == 0)
+        return st;
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (dev != h->device)
+        return fail(LPV_ERR_INVALID_ARG, "handle lives on device %d, current device is %d",
+                    h->device, dev);
+    lpv::LinearCall c = {X, ldx, M, bias, Y, ldy, epi == LPV_EPI_GELU};
+    e = lpv::launch_bsr_linear(h, c, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "bsr_linear launch");
+}
+
+lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                            const void* X, int64_t ldx, int64_t M, const void* bias, void* Y,
+                            int64_t ldy, lpv_epilogue epi, void* stream)
+{
+    const int es = elem_size(dt);
+    if (!es)
+        return fail(LPV_ERR_DTYPE, "unknown element type %d", (int)dt);
+    if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM || N % 16 || K % 16)
+        return fail(LPV_ERR_SHAPE, "weight %lldx%lld: sides must be multiples of 16 in [16, %lld]",
+                    (long long)N, (long long)K, (long long)MAX_DIM);
+    if (!W || ldw < K || (ldw * es) % 16 || !aligned16(W))
+        return fail(LPV_ERR_INVALID_ARG, "W must be non-NULL, 16-byte aligned, ldw >= K and a "
+                                         "multiple of 16 bytes");
+    lpv_status st = check_linear(es, N, K, X, ldx, M, bias, Y, ldy, epi);
+    if (st != LPV_OK || M == 0)
+        return st;
+    lpv::LinearCall c = {X, ldx, M, bias, Y, ldy, epi == LPV_EPI_GELU};
+    hipError_t e = lpv::launch_dense_linear(W, ldw, N, K, dt, c, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "dense_linear launch");
+}
+
+void lpv_bsr_destroy(lpv_bsr* h)
+{
+    free_handle(h);
+}
+
+}  // extern "C"

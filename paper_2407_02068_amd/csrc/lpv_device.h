@@ -1,0 +1,86 @@
+// lpv_device.h -- device-side types and helpers shared by the liblpv kernels
+// (gfx950 / CDNA4 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lpv {
+
+// Matrix-core operand and accumulator vectors.
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+// Element types by their lpv_dtype code (1 = fp16, 2 = bf16).  Each one knows
+// its 32x32x16 MFMA with float32 accumulation and its conversions.
+template <int DT> struct Elem;
+
+template <> struct Elem<2> {
+    typedef bf16x8 frag;
+    __device__ static inline f32x16 mma(frag a, frag b, f32x16 c)
+    {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline float to_f32(uint16_t bits)
+    {
+        return __uint_as_float((uint32_t)bits << 16);
+    }
+    // round to nearest even (NaN stays NaN)
+    __device__ static inline uint16_t from_f32(float v)
+    {
+        return __builtin_bit_cast(uint16_t, (__bf16)v);
+    }
+};
+
+template <> struct Elem<1> {
+    typedef f16x8 frag;
+    __device__ static inline f32x16 mma(frag a, frag b, f32x16 c)
+    {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+    __device__ static inline float to_f32(uint16_t bits)
+    {
+        return (float)__builtin_bit_cast(_Float16, bits);
+    }
+    __device__ static inline uint16_t from_f32(float v)
+    {
+        return __builtin_bit_cast(uint16_t, (_Float16)v);
+    }
+};
+
+template <typename F> __device__ inline F as_frag(uint4 v) { return __builtin_bit_cast(F, v); }
+
+// GELU with the exact error function (float32, device erff).
+__device__ inline float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
+
+// Wave-level inclusive prefix sum over the 64 lanes.
+__device__ inline int wave_inclusive_scan(int v)
+{
+    const int lane = threadIdx.x & 63;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+        int u = __shfl_up(v, d, 64);
+        if (lane >= d)
+            v += u;
+    }
+    return v;
+}
+
+__device__ inline int wave_sum(int v)
+{
+#pragma unroll
+    for (int d = 32; d >= 1; d >>= 1)
+        v += __shfl_xor(v, d, 64);
+    return v;
+}
+
+// Number of lanes below this one whose predicate is set, and the wave total.
+__device__ inline int lanes_below(uint64_t ballot)
+{
+    const int lane = threadIdx.x & 63;
+    const uint64_t below = lane ? (ballot & (~0ull >> (64 - lane))) : 0ull;
+    return __popcll(below);
+}
+
+}  // namespace lpv

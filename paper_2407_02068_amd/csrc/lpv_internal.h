@@ -1,0 +1,80 @@
+// lpv_internal.h -- host-side internals of liblpv: the handle, the schedule
+// constants and the kernel launchers (implemented in pack.hip / linear.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "../../include/lpv.h"
+
+namespace lpv {
+
+// Schedule tile: 32 output rows x 32 reduction columns, the operand shape of
+// one pair of 32x32x16 matrix-core instructions.
+constexpr int TILE = 32;
+// Tile rows per group: a workgroup owns one token tile times one group.
+constexpr int GROUP_TILES = 4;
+// Tokens per workgroup.
+constexpr int BM = 256;
+
+struct Plan {  // sizes learnt on the device during pack
+    int32_t nnzb, n_steps, n_tiles, pad;
+};
+
+}  // namespace lpv
+
+struct lpv_bsr {
+    int64_t N, K;
+    int32_t b_r, b_c, R, C;
+    int64_t nnzb;
+    int32_t dtype;  // lpv_dtype
+    int32_t device;
+    void* meta;  // one allocation: row_ptr, group_order, step_ptr, group_tile0, plan
+    // canonical BSR
+    int32_t* row_ptr;  // R + 1
+    int32_t* col_idx;  // nnzb
+    void* values;      // nnzb * b_r * b_c elements
+    // tile schedule (16-bit element types only)
+    int32_t n_tile_rows, n_tile_cols, n_groups;
+    int64_t n_steps, n_tiles;
+    int32_t* group_order;  // n_groups
+    int32_t* step_ptr;     // n_groups + 1
+    int32_t* group_tile0;  // n_groups + 1, first stream tile of each group
+    int32_t* step_col;     // n_steps
+    int32_t* step_bits;    // n_steps
+    int32_t* step_tile;    // n_steps
+    void* stream_vals;     // n_tiles * TILE * TILE elements, operand order
+};
+
+namespace lpv {
+
+struct PackArgs {
+    const void* W;
+    int64_t ldw, N, K;
+    int32_t es;  // element size in bytes
+    int32_t b_r, b_c, R, C;
+    const uint8_t* mask;
+    int32_t n_tile_rows, n_tile_cols, n_groups;
+};
+
+// pack.hip
+hipError_t launch_pack_plan(const PackArgs& a, int32_t* row_ptr, int32_t* step_ptr,
+                            int32_t* group_tile0, int32_t* group_order, Plan* plan,
+                            hipStream_t s);
+hipError_t launch_pack_fill(const PackArgs& a, const lpv_bsr* h, hipStream_t s);
+hipError_t launch_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, hipStream_t s);
+
+// linear.hip
+struct LinearCall {
+    const void* X;
+    int64_t ldx, M;
+    const void* bias;
+    void* Y;
+    int64_t ldy;
+    int gelu;
+};
+hipError_t launch_bsr_linear(const lpv_bsr* h, const LinearCall& c, hipStream_t s);
+hipError_t launch_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, int dtype,
+                               const LinearCall& c, hipStream_t s);
+
+}  // namespace lpv

@@ -1,0 +1,125 @@
+"""The C ABI on the CPU: liblpv.so loads without a GPU, exports every entry
+point that include/lpv.h declares, and rejects bad arguments before any HIP
+call (so these run here, with made-up device addresses that are never read)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lpv.h")
+LIB = os.path.join(ROOT, "paper_2407_02068_amd", "liblpv.so")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(LIB), reason="liblpv.so not built")
+
+OK, INVALID, SHAPE, DTYPE, BLOCK, ALIAS, ALLOC, HIP = 0, -1, -2, -3, -4, -5, -6, -7
+FAKE = 0x7f0000000000  # 16-byte aligned, never dereferenced: every call below fails its checks first
+
+
+def declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(lpv_[a-z_]+)\s*\(", src)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    from paper_2407_02068_amd import lpv
+    return lpv.lib()
+
+
+def test_header_declares_the_boundary():
+    names = declared()
+    for n in ("lpv_bsr_pack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_bsr_export",
+              "lpv_bsr_unpack", "lpv_bsr_destroy", "lpv_bsr_schedule_export"):
+        assert n in names
+
+
+def test_every_declared_symbol_is_exported():
+    lib = ctypes.CDLL(LIB)
+    for name in declared():
+        assert hasattr(lib, name), "liblpv.so does not export %s" % name
+
+
+def test_python_binding_names_match_header():
+    from paper_2407_02068_amd import lpv
+    assert sorted(lpv.EXPORTED) == declared()
+
+
+def test_status_strings(L):
+    for code, name in ((OK, "LPV_OK"), (INVALID, "LPV_ERR_INVALID_ARG"), (SHAPE, "LPV_ERR_SHAPE"),
+                       (DTYPE, "LPV_ERR_DTYPE"), (BLOCK, "LPV_ERR_BLOCK"), (ALIAS, "LPV_ERR_ALIAS"),
+                       (ALLOC, "LPV_ERR_ALLOC"), (HIP, "LPV_ERR_HIP")):
+        assert L.lpv_status_str(code).decode() == name
+
+
+def pack(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, b_r=32, b_c=32, mask=FAKE):
+    out = ctypes.c_void_p(123)
+    st = L.lpv_bsr_pack(W, ldw, N, K, dt, b_r, b_c, mask, None, ctypes.byref(out))
+    if st != OK:
+        assert out.value is None  # *out is cleared on failure
+    return st
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=3), DTYPE), (dict(dt=-1), DTYPE),
+    (dict(b_r=8), BLOCK), (dict(b_c=128), BLOCK), (dict(b_r=48), BLOCK),
+    (dict(N=3072 + 16, b_r=32), SHAPE), (dict(K=768 + 16), SHAPE), (dict(N=0), SHAPE),
+    (dict(N=1 << 17), SHAPE), (dict(K=-32), SHAPE),
+    (dict(W=0), INVALID), (dict(mask=0), INVALID), (dict(W=FAKE + 8), INVALID),
+    (dict(ldw=700), INVALID), (dict(ldw=772), INVALID),
+])
+def test_pack_rejects_bad_arguments(L, kw, want):
+    assert pack(L, **kw) == want
+    assert L.lpv_last_error().decode() != ""
+
+
+def test_pack_null_out(L):
+    assert L.lpv_bsr_pack(FAKE, 768, 3072, 768, 2, 32, 32, FAKE, None, None) == INVALID
+
+
+def test_pack_alloc_failure_is_reported(L, monkeypatch):
+    monkeypatch.setenv("LPV_FAULT_INJECT", "alloc")
+    assert pack(L) == ALLOC
+    assert "allocation" in L.lpv_last_error().decode()
+
+
+def dense(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, X=FAKE + (1 << 32), ldx=768, M=197, bias=0,
+          Y=FAKE + (2 << 32), ldy=3072, epi=0):
+    return L.lpv_dense_linear(W, ldw, N, K, dt, X, ldx, M, bias, Y, ldy, epi, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=7), DTYPE), (dict(N=3000), SHAPE), (dict(K=8), SHAPE), (dict(M=-1), SHAPE),
+    (dict(ldx=767), INVALID), (dict(ldy=3000), INVALID), (dict(ldx=772), INVALID),
+    (dict(X=0), INVALID), (dict(Y=0), INVALID), (dict(X=FAKE + (1 << 32) + 4), INVALID),
+    (dict(bias=FAKE + 2), INVALID), (dict(epi=2), INVALID), (dict(W=0), INVALID),
+    (dict(Y=FAKE + (1 << 32) + 64), ALIAS), (dict(X=FAKE + (2 << 32) + 1024), ALIAS),
+])
+def test_dense_rejects_bad_arguments(L, kw, want):
+    assert dense(L, **kw) == want
+
+
+def test_dense_m0_is_a_noop(L):
+    # M = 0: nothing to do, no HIP call, even with NULL X / Y
+    assert dense(L, M=0, X=0, Y=0) == OK
+
+
+def test_linear_rejects_null_handle(L):
+    assert L.lpv_bsr_linear(None, FAKE, 768, 197, None, FAKE + (1 << 32), 3072, 0, None) == INVALID
+    from paper_2407_02068_amd.lpv import BsrInfo
+    info = BsrInfo()
+    assert L.lpv_bsr_info_get(None, ctypes.byref(info)) == INVALID
+    assert L.lpv_bsr_export(None, None, None, None, None) == INVALID
+    assert L.lpv_bsr_schedule_export(None, None, None, None, None, None, None) == INVALID
+    assert L.lpv_bsr_unpack(None, FAKE, 768, None) == INVALID
+    L.lpv_bsr_destroy(None)  # NULL-safe
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    from paper_2407_02068_amd import lpv
+    monkeypatch.setattr(lpv, "_lib", None)
+    monkeypatch.setattr(lpv, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError, match="not built"):
+        lpv.lib()

@@ -1,0 +1,260 @@
+"""GPU parity of lpv_bsr_linear and lpv_dense_linear against the float64
+oracle, element by element.
+
+Bar: infinity-norm relative error <= 2e-2 (bf16), 5e-3 (fp16), 1e-5 (fp32),
+float32 accumulation.  Small-integer inputs make the result exact in every
+format and order, and then the GPU must match the oracle bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from gpu_util import TOL, TORCH, bits, dev, f64, host, say
+from paper_2407_02068_amd import lpv
+
+pytestmark = pytest.mark.gpu
+
+SHAPES = ((16, 16), (16, 32), (32, 16), (32, 32), (64, 32), (32, 64), (64, 64))
+
+
+def run_bsr(w, X=None, gelu=None):
+    X = w.X if X is None else X
+    h = lpv.bsr_pack(dev(w.W, w.dtype), dev(w.mask), w.b_r, w.b_c)
+    b = None if w.bias is None else dev(w.bias, w.dtype)
+    Y = lpv.bsr_linear(h, dev(X, w.dtype), b, epi="gelu" if (w.gelu if gelu is None else gelu) else None)
+    torch.cuda.synchronize()
+    return h, Y
+
+
+def ref(w, X=None, gelu=None):
+    X = w.X if X is None else X
+    return oracle.linear(X, w.W, w.dtype, w.b_r, w.b_c, w.mask, w.bias,
+                         gelu=w.gelu if gelu is None else gelu)
+
+
+def assert_close(y, r, dtype, what=""):
+    err = oracle.rel_err(y, r)
+    say("  %s rel err %.3e (bar %.0e)" % (what, err, TOL[dtype]))
+    assert err <= TOL[dtype], "%s: relative error %.3e above %.0e" % (what, err, TOL[dtype])
+
+
+def test_tiny_fc1_fp32():
+    w = wl.tiny_fc1()
+    say("tiny_fc1", w.nnzb)
+    _, Y = run_bsr(w)
+    assert_close(f64(Y), ref(w), "f32", "tiny_fc1")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("b_r,b_c", SHAPES)
+@pytest.mark.parametrize("M", [1, 31, 300])
+def test_parity_small(dtype, b_r, b_c, M):
+    # N = 384: 12 tile rows, several groups; K = 320 / 384: 10-12 tile columns
+    K = 384 if b_c == 64 else 320
+    w = wl.custom(30 + b_r + b_c, M, 384, K, b_r, b_c, dtype, "uniform", 50,
+                  gelu=(M == 300))
+    say("parity", dtype, b_r, b_c, M, "nnzb", w.nnzb)
+    _, Y = run_bsr(w)
+    assert_close(f64(Y), ref(w), dtype, w.name)
+
+
+@pytest.mark.parametrize("b_r,b_c", [(16, 16), (32, 32), (64, 64)])
+def test_parity_fp32_blocks(b_r, b_c):
+    w = wl.custom(40, 129, 192, 192, b_r, b_c, "f32", "bernoulli", 50, gelu=True)
+    say("fp32", b_r, b_c)
+    _, Y = run_bsr(w)
+    assert_close(f64(Y), ref(w), "f32", w.name)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("b_r,b_c", [(16, 16), (32, 32), (64, 32)])
+def test_exact_small_integers(dtype, b_r, b_c):
+    """Integer inputs: every partial sum is exact in float32 and the result is
+    exact in the output type, so the order of accumulation cannot matter."""
+    g = np.random.default_rng(50)
+    M, N, K = 300, 256, 320
+    Xf = g.integers(-1, 2, size=(M, K)) * (g.random((M, K)) < 0.2)
+    Wf = g.integers(-2, 3, size=(N, K))
+    bf = g.integers(-8, 9, size=N)
+    mask = (g.random((N // b_r, K // b_c)) < 0.5).astype(np.uint8)
+    w = wl.Linear("exact", dtype, b_r, b_c, wl.quantize(Wf, dtype), mask, wl.quantize(bf, dtype),
+                  False, wl.quantize(Xf, dtype), M)
+    r = ref(w)
+    assert np.max(np.abs(r)) < 256  # exact in bf16
+    say("exact", dtype, b_r, b_c)
+    _, Y = run_bsr(w)
+    assert np.array_equal(f64(Y), r)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_dense_path(dtype):
+    w = wl.custom(60, 300, 384, 320, 32, 32, dtype, "all", 0, gelu=True)
+    say("dense", dtype)
+    Y = lpv.dense_linear(dev(w.W, dtype), dev(w.X, dtype), dev(w.bias, dtype), epi="gelu")
+    torch.cuda.synchronize()
+    assert_close(f64(Y), ref(w), dtype, "dense")
+    # the block-sparse path with every block kept computes the same thing
+    _, Ys = run_bsr(w)
+    assert_close(f64(Ys), ref(w), dtype, "all-kept bsr")
+
+
+def test_dense_fp32():
+    w = wl.custom(61, 70, 64, 96, 32, 32, "f32", "all", 0)
+    Y = lpv.dense_linear(dev(w.W, "f32"), dev(w.X, "f32"), dev(w.bias, "f32"))
+    torch.cuda.synchronize()
+    assert_close(f64(Y), ref(w), "f32", "dense fp32")
+
+
+@pytest.mark.parametrize("gelu", [False, True])
+def test_no_kept_block_gives_bias(gelu):
+    w = wl.custom(62, 257, 256, 192, 32, 32, "bf16", "none", 100, gelu=gelu)
+    say("none kept", gelu)
+    h, Y = run_bsr(w)
+    assert h.info["nnzb"] == 0
+    r = ref(w)
+    if gelu:
+        assert_close(f64(Y), r, "bf16", "gelu(bias)")
+    else:
+        assert np.array_equal(f64(Y), r)  # bias is a bf16 value: exact
+    w.bias = None
+    _, Y0 = run_bsr(w)
+    assert torch.count_nonzero(Y0).item() == 0
+
+
+def test_nonfinite_dropped_blocks_do_not_leak():
+    w = wl.custom(63, 200, 256, 256, 32, 32, "bf16", "uniform", 50)
+    _, Y = run_bsr(w)
+    exp = np.kron(w.mask, np.ones((32, 32), np.uint8)) == 0
+    W2 = w.W.copy()
+    W2[exp] = wl.quantize(np.array([np.nan], np.float32), "bf16")[0]
+    W2[exp & (np.arange(256)[None, :] % 3 == 0)] = wl.quantize(np.array([np.inf], np.float32), "bf16")[0]
+    w2 = wl.Linear("nan", "bf16", 32, 32, W2, w.mask, w.bias, False, w.X, w.M)
+    _, Y2 = run_bsr(w2)
+    assert torch.isfinite(Y2.float()).all()
+    assert torch.equal(Y.view(torch.int16), Y2.view(torch.int16))
+
+
+def test_deterministic_and_token_permutation():
+    w = wl.custom(64, 700, 384, 320, 32, 32, "bf16", "zipf", 40, gelu=True)
+    h, Y1 = run_bsr(w)
+    b = dev(w.bias, "bf16")
+    X = dev(w.X, "bf16")
+    Y2 = lpv.bsr_linear(h, X, b, epi="gelu")
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        Y3 = lpv.bsr_linear(h, X, b, epi="gelu")
+    torch.cuda.synchronize()
+    assert torch.equal(Y1.view(torch.int16), Y2.view(torch.int16))
+    assert torch.equal(Y1.view(torch.int16), Y3.view(torch.int16))
+    perm = torch.from_numpy(np.random.default_rng(5).permutation(700)).cuda()
+    Yp = lpv.bsr_linear(h, X[perm].contiguous(), b, epi="gelu")
+    torch.cuda.synchronize()
+    assert torch.equal(Yp.view(torch.int16), Y1[perm].view(torch.int16))
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_strided_views_and_guard_bands(dtype):
+    """X read through a column slice of a wider buffer (ldx > K); Y written
+    into the middle of a padded buffer (ldy > N) whose canaries must survive."""
+    w = wl.custom(65, 197, 256, 192, 32, 16 if dtype == "f32" else 32, dtype, "uniform", 40)
+    tt = TORCH[dtype]
+    big = torch.zeros((w.M, 3 * w.K), dtype=tt, device="cuda")
+    big[:, w.K:2 * w.K] = dev(w.X, dtype)
+    Xv = big[:, w.K:2 * w.K]
+    ldy = w.N + 64
+    canary = torch.full((w.M + 2, ldy), -7.0, dtype=tt, device="cuda")
+    Yv = canary[1:w.M + 1, :w.N]
+    h = lpv.bsr_pack(dev(w.W, dtype), dev(w.mask), w.b_r, w.b_c)
+    lpv.bsr_linear(h, Xv, dev(w.bias, dtype), Y=Yv)
+    torch.cuda.synchronize()
+    assert_close(f64(Yv), ref(w), dtype, "strided")
+    c = canary.float().cpu()
+    assert torch.all(c[0] == -7) and torch.all(c[-1] == -7) and torch.all(c[:, w.N:] == -7)
+
+
+def test_m_zero_is_noop():
+    w = wl.custom(66, 1, 64, 64, 32, 32, "bf16", "uniform", 50)
+    h = lpv.bsr_pack(dev(w.W, "bf16"), dev(w.mask), 32, 32)
+    Y = lpv.bsr_linear(h, torch.empty((0, 64), dtype=torch.bfloat16, device="cuda"))
+    assert Y.shape == (0, 64)
+
+
+def test_rejects_aliasing_and_wrong_device_layouts():
+    w = wl.custom(67, 64, 64, 64, 32, 32, "bf16", "uniform", 50)
+    h = lpv.bsr_pack(dev(w.W, "bf16"), dev(w.mask), 32, 32)
+    buf = torch.zeros((64, 128), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(lpv.LpvError) as e:
+        lpv.bsr_linear(h, buf[:, :64], Y=buf[:, 64:])
+    assert e.value.status == -5
+    with pytest.raises(lpv.LpvError):
+        lpv.bsr_linear(h, buf[:, 1:65])  # misaligned X
+
+
+def _sampled_rows(M, n=64, seed=0):
+    g = np.random.default_rng(seed)
+    rows = set(range(min(n, M))) | set(range(max(0, M - n), M))
+    rows |= set(g.choice(M, size=min(n, M), replace=False).tolist())
+    return np.array(sorted(rows))
+
+
+def _full_size(w, gelu=None, seed=0):
+    """Full-size run (the benchmark's launch configuration), checked on
+    sampled token rows (first, last including the tail, random)."""
+    say("full size", w.name, "M", w.M, "nnzb", w.nnzb)
+    _, Y = run_bsr(w, gelu=gelu)
+    rows = _sampled_rows(w.M, seed=seed)
+    r = ref(w, X=w.X[rows], gelu=gelu)
+    y = f64(Y[torch.from_numpy(rows).cuda()])
+    assert_close(y, r, w.dtype, w.name + " sampled")
+    return Y
+
+
+def test_full_headline_fc1():
+    _full_size(wl.b_fc1())
+
+
+def test_full_headline_fc1_fp16_gelu():
+    _full_size(wl.b_fc1(dtype="f16", gelu=True))
+
+
+def test_full_s_fc1_gelu():
+    _full_size(wl.s_fc1_gelu())
+
+
+def test_full_b_layer():
+    for w in wl.b_layer():
+        _full_size(w)
+
+
+@pytest.mark.parametrize("block", [16, 64])
+def test_full_fc1_other_blocks(block):
+    _full_size(wl.b_fc1(block=block, sparsity=75))
+
+
+def test_full_dense_headline_shape():
+    w = wl.b_fc1(sparsity=0)
+    say("dense full", w.name)
+    Y = lpv.dense_linear(dev(w.W, "bf16"), dev(w.X, "bf16"), dev(w.bias, "bf16"))
+    torch.cuda.synchronize()
+    rows = _sampled_rows(w.M)
+    r = oracle.linear(w.X[rows], w.W, "bf16", 32, 32, np.ones_like(w.mask), w.bias)
+    assert_close(f64(Y[torch.from_numpy(rows).cuda()]), r, "bf16", "dense full sampled")
+
+
+def test_chain_b_stack_links():
+    """The DeiT-B stack (qkv -> V third -> proj -> fc1 + GELU -> fc2) with
+    skewed (Zipf) masks, 2 layers at 2 images; each link is checked against
+    the oracle fed the GPU's own input to that link."""
+    layers = wl.b_stack(M=2 * 197, layers=2)
+    X = dev(layers[0].X, "bf16")
+    for w in layers:
+        h = lpv.bsr_pack(dev(w.W, "bf16"), dev(w.mask), 32, 32)
+        Xin = X[:, 1536:2304] if w.name.endswith("proj") else X
+        Y = lpv.bsr_linear(h, Xin, dev(w.bias, "bf16"), epi="gelu" if w.gelu else None)
+        torch.cuda.synchronize()
+        xin = host(Xin.contiguous(), "bf16")
+        r = oracle.linear(xin, w.W, "bf16", 32, 32, w.mask, w.bias, gelu=w.gelu)
+        assert_close(f64(Y), r, "bf16", w.name)
+        X = Y
