@@ -100,7 +100,7 @@ void free_handle(lpv_bsr* h)
     if (!h)
         return;
     void* bufs[] = {h->meta, h->col_idx, h->values, h->step_col, h->step_bits, h->step_tile,
-                    h->stream_vals};
+                    h->step_meta, h->stream_vals};
     for (void* p : bufs)
         if (p)
             (void)hipFree(p);
@@ -230,7 +230,14 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
         if (e == hipSuccess)
             e = dmalloc((void**)&h->step_tile, (size_t)h->n_steps * sizeof(int32_t));
         if (e == hipSuccess)
-            e = dmalloc(&h->stream_vals, (size_t)h->n_tiles * lpv::TILE * lpv::TILE * es);
+            e = dmalloc((void**)&h->step_meta, (size_t)h->n_steps * sizeof(int2));
+        if (e == hipSuccess)
+            e = dmalloc(&h->stream_vals,
+                        (size_t)(h->n_tiles + lpv::GROUP_TILES) * lpv::TILE * lpv::TILE * es);
+        // the linear kernel's DMA reads up to GROUP_TILES tiles past a step's own
+        if (e == hipSuccess)
+            e = hipMemsetAsync((char*)h->stream_vals + (size_t)h->n_tiles * lpv::TILE * lpv::TILE * es,
+                               0, (size_t)lpv::GROUP_TILES * lpv::TILE * lpv::TILE * es, s);
     }
     if (e != hipSuccess) {
         free_handle(h);

@@ -1,24 +1,34 @@
 // linear.hip -- Y = g(X W~^T + b): the block-sparse hot path and the dense
 // reference path.
 //
-// bf16 / fp16 (matrix cores).  A workgroup of 4 waves owns one tile of BM = 256
-// tokens times one group of GROUP_TILES x 32 output rows.  It walks the
-// group's steps (the 32-wide reduction columns where any of its rows keeps a
-// tile; pruned columns are never touched):
-//   1. the X slice [256 tokens x 32 columns] and the step's kept W tiles are
-//      loaded from HBM with 16-byte coalesced loads and staged in LDS (double
-//      buffered: step s+1 is in flight while step s computes);
-//   2. each wave takes 64 tokens and, for every kept tile of the step, issues
-//      v_mfma_f32_32x32x16 (bf16 or fp16 in, float32 accumulate) into its
-//      accumulator for that tile row.
-// The work per workgroup is therefore proportional to the kept tiles, the
-// quantity the paper's cost model counts (Sec. 3.4).  The epilogue adds the
-// bias, applies GELU if asked, rounds once to the element type and stores Y
-// through LDS so every row segment goes out as full 128-byte lines.
+// bf16 / fp16 (matrix cores).  The work is cut into items: one tile of BM = 256
+// tokens times one group of GROUP_TILES = 8 tile rows (256 output features).
+// An item walks its group's steps -- the 32-wide reduction columns where any
+// of its rows keeps a tile; other columns are never touched -- so its work is
+// proportional to the kept tiles, the quantity the paper's cost model counts
+// (Sec. 3.4).
+//
+// One persistent workgroup of 8 waves per compute unit takes items in turn
+// (consecutive items, which share a token tile, go to workgroups on the same
+// XCD so the X slice is fetched from HBM once per XCD L2).  Its steps, across
+// item boundaries, flow through a 4-slot LDS ring:
+//   - gfx950 global->LDS DMA (global_load_lds_dwordx4) stages each step's X
+//     slice [256 tokens x 32 columns] and kept W tiles, 3 steps ahead, with
+//     16-byte coalesced loads and no registers in between; every wave issues
+//     the same number of DMA instructions per step (rows or tiles past the
+//     operands read a zero line), so a fixed vmcnt wait tells a wave that its
+//     part of a step has landed, and one barrier per step tells everyone;
+//   - wave (m, h) takes tokens [64m, 64m + 64) and tile rows [4h, 4h + 4) of
+//     the group and issues v_mfma_f32_32x32x16 (bf16 / fp16 in, float32
+//     accumulate) for each kept tile; the two waves of a SIMD cover both row
+//     halves, so every SIMD gets the step's whole kept count.
+// The epilogue adds the bias (scalar loads), applies GELU if asked, rounds once
+// to the element type and stores Y straight from the accumulators, while the
+// DMA of the next item's first steps is already in flight.
 //
 // MFMA operand roles: A = a W tile (rows = output features), B = X slice
-// transposed (columns = tokens), so D[n][token]; lane l then holds token l % 32
-// and, per group of 4 accumulator registers, 4 consecutive output features.
+// transposed (columns = tokens), so D[n][token]: lane l holds token l % 32 and,
+// per group of 4 accumulator registers, 4 consecutive output features.
 //
 // The dense path is the same kernel with every tile kept and W read straight
 // from its row-major layout.  fp32 runs a plain VALU kernel over the canonical
@@ -29,234 +39,413 @@
 namespace lpv {
 namespace {
 
-constexpr int NT = 256;       // threads per workgroup (4 waves)
-constexpr int XROW = 5;       // uint4 per staged X row: 64 bytes of data + 16 bytes pad
-constexpr int TILE_U4 = 128;  // uint4 per 32x32 16-bit tile
-constexpr int EROW = 9;       // uint4 per epilogue row: 128 bytes + 16 bytes pad
+constexpr int NT = 512;             // threads per workgroup: 8 waves
+constexpr int G = GROUP_TILES;      // tile rows per item
+constexpr int NS = 4;               // LDS ring slots
+constexpr int D = NS - 1;           // DMA runs D steps ahead of the matrix cores
+constexpr int XU4 = BM * 4;         // 16-byte chunks of one X slice (256 x 32 elements)
+constexpr int WU4 = G * 128;        // 16-byte chunks of G W tiles (32 x 32 elements each)
+constexpr int SLOT = XU4 + WU4;     // one ring slot: 32 KB
+constexpr int NSTORE = 16;          // store instructions per wave per item
+constexpr int EPI_U4 = 64 * 4;      // per-wave epilogue tile: 64 rows x 64 bytes
+constexpr int LPS = 4;              // DMA instructions per wave per step (2 X + 2 W)
+constexpr int WAIT_A = LPS * (D - 1);        // DMA still allowed in flight at a step
+constexpr int WAIT_B = WAIT_A + NSTORE;      // ... when an item's stores were issued since
 
-struct Args {
-    const char* X;
-    int64_t ldx, M, K, N;
-    // sparse operand stream and schedule
-    const uint4* stream;
-    const int32_t* step_ptr;
-    const int32_t* step_col;
-    const int32_t* step_bits;
-    const int32_t* step_tile;
-    const int32_t* group_order;
-    // dense weight
-    const char* W;
-    int64_t ldw;
-    int32_t n_groups, n_tile_rows, n_tile_cols, n_mtiles;
-    const char* bias;
-    char* Y;
-    int64_t ldy;
+static_assert(XU4 == 2 * 8 * 64 && WU4 == 2 * 8 * 64, "2 X and 2 W DMA instructions per wave");
+static_assert((NS * SLOT + 8 * EPI_U4) * 16 <= 163840, "LDS budget of one workgroup");
+
+// A zero line for DMA lanes outside X (token or column tails), and a sink for
+// store lanes outside Y: the instruction count of a wave never depends on
+// where the operands end.
+static __device__ uint4 g_zero[1];
+static __device__ uint4 g_sink[64];
+
+// Sizes of one call (the arrays are separate __restrict__ kernel arguments,
+// so the schedule and bias reads can go through the scalar cache).
+struct Dims {
+    int64_t ldx, M, K, N, ldw, ldy;
+    int32_t n_groups, n_tile_rows, n_tile_cols, n_items;
 };
 
-constexpr int G = GROUP_TILES;
-constexpr int SMEM_MAIN = 2 * BM * XROW + 2 * G * TILE_U4;
-constexpr int SMEM_EPI = 4 * 64 * EROW;
-constexpr int SMEM_U4 = SMEM_MAIN > SMEM_EPI ? SMEM_MAIN : SMEM_EPI;
+struct Args {
+    Dims d;
+    const char* X;
+    const uint4* stream;       // sparse operand stream
+    const int32_t* step_ptr;
+    const int2* step_meta;
+    const int32_t* group_order;
+    const char* W;             // dense weight
+    const char* bias;
+    char* Y;
+};
 
-template <int DT, bool GELU, bool DENSE>
-__global__ __launch_bounds__(NT, 2) void k_linear16(Args a)
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+__device__ inline void dma16(const void* src, uint4* lds_wave_base)
+{
+    __builtin_amdgcn_global_load_lds(src, (lds_ptr)lds_wave_base, 16, 0, 0);
+}
+
+// s_waitcnt vmcnt(n) lgkmcnt(0) (gfx9 encoding; expcnt left alone)
+template <int N> __device__ inline void wait_vm_lgkm0()
+{
+    static_assert(N < 64, "vmcnt is 6 bits");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+}
+
+// The same with a wave-uniform count: s_waitcnt only takes an immediate, so
+// dispatch over the counts the ring can produce (larger ones wait for more,
+// which is always safe).
+__device__ inline void wait_vm_lgkm0_dyn(int n)
+{
+#define LPV_W(N)                  \
+    case N:                       \
+        wait_vm_lgkm0<N>();       \
+        break;
+    switch (n) {
+        LPV_W(0) LPV_W(1) LPV_W(2) LPV_W(3) LPV_W(4) LPV_W(5) LPV_W(6) LPV_W(7) LPV_W(8)
+        LPV_W(9) LPV_W(10) LPV_W(11) LPV_W(12) LPV_W(13) LPV_W(14) LPV_W(15) LPV_W(16)
+        LPV_W(17) LPV_W(18) LPV_W(19) LPV_W(20) LPV_W(21) LPV_W(22) LPV_W(23) LPV_W(24)
+        LPV_W(25) LPV_W(26) LPV_W(27) LPV_W(28)
+    default:
+        wait_vm_lgkm0<28>();
+        break;
+    }
+#undef LPV_W
+}
+
+__device__ inline void barrier_step()
+{
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+}
+
+// 16-byte LDS read issued from inline assembly: the compiler then does not
+// treat it as a read of LDS that the in-flight DMA may be writing (it would
+// otherwise drain all DMA before every read).  The ring protocol (vmcnt wait +
+// barrier per step) is what orders these reads after the DMA that fills them,
+// and lds_wait() below after the reads themselves.
+typedef int v4i __attribute__((ext_vector_type(4)));
+
+__device__ inline uint32_t lds_addr(const void* p)
+{
+    return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
+template <int OFF> __device__ inline v4i lds_read16(uint32_t addr)
+{
+    v4i r;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+    return r;
+}
+
+__device__ inline void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
+
+__device__ inline void lds_write8(uint32_t addr, uint2 v)
+{
+    asm volatile("ds_write_b64 %0, %1" : : "v"(addr), "v"(v) : "memory");
+}
+
+// After lds_wait(): tie a value read by lds_read16 to that point, so its uses
+// cannot move above the wait.
+__device__ inline void after_wait(v4i& a) { asm volatile("" : "+v"(a)); }
+
+// X slice layout in LDS: chunk (row r, 16-byte column chunk ch) at r * 4 + (ch ^ swz(r)).
+__device__ inline int xswz(int r) { return (r >> 1) & 3; }
+// Epilogue tile layout (64 rows of 64 bytes): chunk c of row r at c ^ eswz(r).
+__device__ inline int eswz(int r) { return (r >> 1) & 3; }
+
+template <int DT, bool GELU, bool DENSE, bool KTAIL>
+__global__ __launch_bounds__(NT, 1) void k_linear16(
+    const Dims a, const char* __restrict__ X, const uint4* __restrict__ stream,
+    const int32_t* __restrict__ step_ptr, const int2* __restrict__ step_meta,
+    const int32_t* __restrict__ group_order, const char* __restrict__ W,
+    const uint32_t* __restrict__ bias32, char* __restrict__ Y)
 {
     using E = Elem<DT>;
     using F = typename E::frag;
-    __shared__ uint4 smem[SMEM_U4];
-    uint4* xs = smem;                 // [2][BM * XROW]
-    uint4* ws = smem + 2 * BM * XROW; // [2][G * TILE_U4]
+    __shared__ uint4 smem[NS * SLOT + NT / 64 * EPI_U4];
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
+    const int wm = wave & 3, wh = wave >> 2;
 
-    // Work item of this workgroup.  Consecutive workgroups go to different
-    // XCDs (round robin over 8), so hand each XCD a contiguous run of items:
-    // the groups of one token tile then share that XCD's L2 for their X reads.
-    const int n_items = a.n_mtiles * a.n_groups;
-    const int per_xcd = (int)(gridDim.x >> 3);
-    const int item = (int)(blockIdx.x & 7) * per_xcd + (int)(blockIdx.x >> 3);
-    if (item >= n_items)
+    // this workgroup's items: k * P + item_off, k = 0, 1, ...
+    const int P = (int)gridDim.x;
+    const int item_off = (int)(blockIdx.x & 7) * (P >> 3) + (int)(blockIdx.x >> 3);
+    const int my_items = item_off < a.n_items ? (a.n_items - item_off + P - 1) / P : 0;
+    if (my_items == 0)
         return;
-    const int mt = item / a.n_groups;
-    const int gs = item - mt * a.n_groups;
-    const int g = DENSE ? gs : a.group_order[gs];
-    const int s_begin = DENSE ? 0 : a.step_ptr[g];
-    const int s_end = DENSE ? a.n_tile_cols : a.step_ptr[g + 1];
-    const int64_t m0 = (int64_t)mt * BM;
-    const int row0 = g * G;
-    const int rows_valid = min(G, a.n_tile_rows - row0);
 
-    f32x16 acc[2][G];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int j = 0; j < G; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v)
-                acc[t][j][v] = 0.0f;
+    const char* zero = (const char*)g_zero;
+    const int last_col = a.n_tile_cols - 1;
+    const uint32_t smem0 = lds_addr(smem);
 
-    // ---- global -> registers for one step
-    uint4 xr[4];
-    uint4 wr[G / 2];
-    int bits_next = 0;
-    auto fetch = [&](int s) {
-        const int col = DENSE ? s : a.step_col[s];
-        const int bits = DENSE ? ((1 << rows_valid) - 1) : a.step_bits[s];
-        bits_next = bits;
+    // Per-lane constants of this wave's DMA instructions.  X: LDS chunk p of
+    // the slice holds row p / 4, column chunk (p % 4) ^ swz(row).  W: chunk q
+    // of the step's operand-order tiles (dense: tile q / 128, lane q % 64 of
+    // k-step (q / 64) % 2).
+    int xrow[2], xcol[2], wrow[2], wcol[2];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int idx = i * NT + tid;
-            const int r = idx >> 2, ch = idx & 3;
-            const int64_t m = m0 + r;
-            const int64_t k = (int64_t)col * TILE + ch * 8;
-            xr[i] = make_uint4(0, 0, 0, 0);
-            if (m < a.M && k < a.K)
-                xr[i] = *(const uint4*)(a.X + (m * a.ldx + k) * 2);
-        }
+    for (int i = 0; i < 2; ++i) {
+        const int p = (wave * 2 + i) * 64 + lane;
+        xrow[i] = p >> 2;
+        xcol[i] = ((p & 3) ^ xswz(p >> 2)) * 8;
+        wrow[i] = (p >> 7) * TILE + (p & 31);
+        wcol[i] = ((p >> 6) & 1) * 16 + ((p >> 5) & 1) * 8;
+    }
+
+    auto group_of = [&](int k, int& g, int& mt) {
+        const int it = k * P + item_off;
+        mt = it / a.n_groups;
+        const int gs = it - mt * a.n_groups;
+        g = DENSE ? gs : group_order[gs];
+    };
+    auto steps_of = [&](int g, int& s0, int& s1) {
         if (DENSE) {
-#pragma unroll
-            for (int i = 0; i < G / 2; ++i) {
-                const int idx = i * NT + tid;
-                const int rr = idx >> 2, ch = idx & 3;
-                const int64_t n = (int64_t)row0 * TILE + rr;
-                const int64_t k = (int64_t)col * TILE + ch * 8;
-                wr[i] = make_uint4(0, 0, 0, 0);
-                if (n < a.N && k < a.K)
-                    wr[i] = *(const uint4*)(a.W + (n * a.ldw + k) * 2);
-            }
+            s0 = 0;
+            s1 = a.n_tile_cols;
         } else {
-            const int nk = __popc(bits);
-            const uint4* src = a.stream + (int64_t)a.step_tile[s] * TILE_U4;
+            s0 = step_ptr[g];
+            s1 = step_ptr[g + 1];
+        }
+    };
+
+    // ---- producer: the DMA cursor runs D steps ahead, across items.  Every
+    // wave issues exactly 2 X and 2 W DMA instructions per step: X rows past M
+    // repeat row M - 1 (their outputs are never stored); W chunks past the
+    // step's kept tiles fetch the tiles that follow (the stream is padded), and
+    // land in slot space nobody reads.
+    int pk = -1, ps = 0, ps_end = 0;
+    const char* xsrc[2];  // X[min(m0 + row, M - 1)][col chunk] at column tile 0
+    const char* wsrc[2];  // dense: W[min(g * 256 + row, N - 1)][col chunk]
+    auto next_item = [&]() {
+        while (++pk < my_items) {
+            int g, mt;
+            group_of(pk, g, mt);
+            steps_of(g, ps, ps_end);
+            if (ps < ps_end) {
 #pragma unroll
-            for (int i = 0; i < G / 2; ++i) {
-                const int idx = i * NT + tid;
-                if (idx < nk * TILE_U4)
-                    wr[i] = src[idx];
+                for (int i = 0; i < 2; ++i) {
+                    const int64_t m = min((int64_t)mt * BM + xrow[i], a.M - 1);
+                    xsrc[i] = X + (m * a.ldx + xcol[i]) * 2;
+                    const int64_t n = min((int64_t)g * G * TILE + wrow[i], a.N - 1);
+                    wsrc[i] = DENSE ? W + (n * a.ldw + wcol[i]) * 2 : zero;
+                }
+                return;
             }
         }
     };
-    // ---- registers -> LDS buffer
-    auto commit = [&](int buf) {
-        uint4* xb = xs + buf * BM * XROW;
-        uint4* wb = ws + buf * G * TILE_U4;
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int idx = i * NT + tid;
-            xb[(idx >> 2) * XROW + (idx & 3)] = xr[i];
-        }
-        if (DENSE) {
-            // row rr, 16-byte chunk ch of the group's W rows -> operand order
-#pragma unroll
-            for (int i = 0; i < G / 2; ++i) {
-                const int idx = i * NT + tid;
-                const int rr = idx >> 2, ch = idx & 3;
-                const int j = rr >> 5, l = (rr & 31) + 32 * (ch & 1), ks = ch >> 1;
-                wb[j * TILE_U4 + ks * 64 + l] = wr[i];
+    // `meta` is step_meta[ps], loaded by the caller ahead of time (sparse only)
+    auto produce = [&](int slot, int2 meta) {
+        const uint4* xdst = smem + slot * SLOT + wave * 128;
+        const uint4* wdst = smem + slot * SLOT + XU4 + wave * 128;
+        if (pk < my_items) {
+            const int col = DENSE ? ps : (meta.x & 0xffff);
+            const int64_t coff = (int64_t)col * TILE * 2;  // bytes to column tile col
+            const char* xs0 = xsrc[0] + coff;
+            const char* xs1 = xsrc[1] + coff;
+            const char *ws0, *ws1;
+            if (DENSE) {
+                ws0 = wsrc[0] + coff;
+                ws1 = wsrc[1] + coff;
+            } else {
+                const char* tiles = (const char*)stream + (int64_t)meta.y * 2048 + wave * 2048;
+                ws0 = tiles + lane * 16;
+                ws1 = tiles + 1024 + lane * 16;
             }
+            if (KTAIL && col == last_col) {  // columns past K read the zero line
+                if (col * TILE + xcol[0] >= a.K) xs0 = zero;
+                if (col * TILE + xcol[1] >= a.K) xs1 = zero;
+                if (DENSE && col * TILE + wcol[0] >= a.K) ws0 = zero;
+                if (DENSE && col * TILE + wcol[1] >= a.K) ws1 = zero;
+            }
+            dma16(xs0, (uint4*)xdst);
+            dma16(xs1, (uint4*)xdst + 64);
+            dma16(ws0, (uint4*)wdst);
+            dma16(ws1, (uint4*)wdst + 64);
+            if (++ps >= ps_end)
+                next_item();
         } else {
-            const int nk = __popc(bits_next);
-#pragma unroll
-            for (int i = 0; i < G / 2; ++i) {
-                const int idx = i * NT + tid;
-                if (idx < nk * TILE_U4)
-                    wb[idx] = wr[i];
-            }
+            // past the last step: the same instruction count, into a free slot
+            dma16(zero, (uint4*)xdst);
+            dma16(zero, (uint4*)xdst + 64);
+            dma16(zero, (uint4*)wdst);
+            dma16(zero, (uint4*)wdst + 64);
         }
     };
-    // ---- LDS -> matrix cores
-    auto compute = [&](int buf, int bits) {
-        const uint4* xb = xs + buf * BM * XROW;
-        const uint4* wb = ws + buf * G * TILE_U4;
-        F xa[2][2];
+
+    next_item();
+    int2 pmeta = make_int2(0, 0);  // step_meta at the producer cursor
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+    for (int i = 0; i < D; ++i) {
+        if (!DENSE)
+            pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
+        produce(i, pmeta);
+    }
+    if (!DENSE)
+        pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
+
+    // LDS read addresses of this lane (slot 0; u = 1 is +2048 bytes, W ks = 1 is +1024)
+    uint32_t xa_addr[2];
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+        const int r = wm * 64 + (lane & 31);
+        const int ch = ks * 2 + (lane >> 5);
+        xa_addr[ks] = smem0 + (r * 4 + (ch ^ xswz(r))) * 16;
+    }
+    const uint32_t wa_addr = smem0 + XU4 * 16 + lane * 16;
+    const uint32_t ebase = smem0 + NS * SLOT * 16 + wave * (EPI_U4 * 16);
+
+    f32x16 acc[2][4];
+    int t = 0;  // steps consumed
+    for (int ck = 0; ck < my_items; ++ck) {
+        int g, mt, s0, s1;
+        group_of(ck, g, mt);
+        steps_of(g, s0, s1);
+        const int rows = (1 << min(G, a.n_tile_rows - g * G)) - 1;
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int v = 0; v < 16; ++v)
+                    acc[u][j][v] = 0.0f;
+
+        // one step: wait for its DMA, let the producer refill the freed slot,
+        // then LDS -> matrix cores.  During an item's first D steps the
+        // previous epilogue's NSTORE stores may still be in flight too.  The
+        // metadata of the next step (the consumer's bits, the producer's column
+        // and tile) is loaded a step ahead, so its latency hides behind the
+        // matrix cores.
+        int bits = DENSE ? rows : (s0 < s1 ? (step_meta[s0].x >> 16) : 0);
+        auto step = [&](int s, bool after_epilogue) {
+            if (after_epilogue)
+                wait_vm_lgkm0<WAIT_B>();
+            else
+                wait_vm_lgkm0<WAIT_A>();
+            barrier_step();
+            produce((t + D) & (NS - 1), pmeta);
+            if (!DENSE) {
+                pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
+            }
+            const int cur = bits;
+            if (!DENSE)
+                bits = s + 1 < s1 ? (step_meta[s + 1].x >> 16) : 0;
+
+            const uint32_t slot_off = (uint32_t)(t & (NS - 1)) * (SLOT * 16);
+            // all of this step's operand reads first, one wait, then the matrix cores
+            v4i xa[2][2], wf[4][2];
 #pragma unroll
             for (int ks = 0; ks < 2; ++ks) {
-                const int r = wave * 64 + t * 32 + (lane & 31);
-                xa[t][ks] = as_frag<F>(xb[r * XROW + ks * 2 + (lane >> 5)]);
+                xa[0][ks] = lds_read16<0>(xa_addr[ks] + slot_off);
+                xa[1][ks] = lds_read16<2048>(xa_addr[ks] + slot_off);
             }
-        int idx = 0;
+            const int bh = (cur >> (4 * wh)) & 15;
+            uint32_t wa = wa_addr + slot_off + (wh ? __popc(cur & 15) * 2048 : 0);
 #pragma unroll
-        for (int j = 0; j < G; ++j) {
-            if (bits & (1 << j)) {
-                const F w0 = as_frag<F>(wb[idx * TILE_U4 + lane]);
-                const F w1 = as_frag<F>(wb[idx * TILE_U4 + 64 + lane]);
-                acc[0][j] = E::mma(w0, xa[0][0], acc[0][j]);
-                acc[1][j] = E::mma(w0, xa[1][0], acc[1][j]);
-                acc[0][j] = E::mma(w1, xa[0][1], acc[0][j]);
-                acc[1][j] = E::mma(w1, xa[1][1], acc[1][j]);
-                ++idx;
-            }
-        }
-    };
-
-    if (s_begin < s_end) {
-        fetch(s_begin);
-        commit(0);
-    }
-    __syncthreads();
-    for (int s = s_begin; s < s_end; ++s) {
-        const int buf = (s - s_begin) & 1;
-        const int bits = bits_next;
-        if (s + 1 < s_end)
-            fetch(s + 1);
-        compute(buf, bits);
-        if (s + 1 < s_end)
-            commit(buf ^ 1);
-        __syncthreads();
-    }
-
-    // ---- epilogue: bias, GELU, one rounding, transpose through LDS, store
-    uint4* eb = smem + wave * 64 * EROW;
-    uint2* eb2 = (uint2*)eb;
-#pragma unroll
-    for (int jp = 0; jp < G; jp += 2) {
-        if (jp >= rows_valid)
-            break;
-#pragma unroll
-        for (int jj = 0; jj < 2; ++jj) {
-            const int j = jp + jj;
-            const int64_t n_tile = (int64_t)(row0 + j) * TILE;
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int n_off = 8 * q + 4 * (lane >> 5);
-                float b[4] = {0.f, 0.f, 0.f, 0.f};
-                if (a.bias && n_tile + n_off < a.N) {
-                    const uint2 bb = *(const uint2*)(a.bias + (n_tile + n_off) * 2);
-                    b[0] = E::to_f32(bb.x & 0xffff);
-                    b[1] = E::to_f32(bb.x >> 16);
-                    b[2] = E::to_f32(bb.y & 0xffff);
-                    b[3] = E::to_f32(bb.y >> 16);
+            for (int j = 0; j < 4; ++j) {
+                if (bh & (1 << j)) {
+                    wf[j][0] = lds_read16<0>(wa);
+                    wf[j][1] = lds_read16<1024>(wa);
+                    wa += 2048;
                 }
+            }
+            lds_wait();
 #pragma unroll
-                for (int t = 0; t < 2; ++t) {
-                    float v[4];
+            for (int u = 0; u < 2; ++u)
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        v[e] = acc[t][j][4 * q + e] + b[e];
-                        if (GELU)
-                            v[e] = gelu_erf(v[e]);
+                for (int ks = 0; ks < 2; ++ks)
+                    after_wait(xa[u][ks]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (bh & (1 << j)) {
+                    after_wait(wf[j][0]);
+                    after_wait(wf[j][1]);
+                    const F w0 = __builtin_bit_cast(F, wf[j][0]);
+                    const F w1 = __builtin_bit_cast(F, wf[j][1]);
+                    acc[0][j] = E::mma(w0, __builtin_bit_cast(F, xa[0][0]), acc[0][j]);
+                    acc[1][j] = E::mma(w0, __builtin_bit_cast(F, xa[1][0]), acc[1][j]);
+                    acc[0][j] = E::mma(w1, __builtin_bit_cast(F, xa[0][1]), acc[0][j]);
+                    acc[1][j] = E::mma(w1, __builtin_bit_cast(F, xa[1][1]), acc[1][j]);
+                }
+            }
+            ++t;
+        };
+        // the first D steps of every item but the first wait past the stores of
+        // the epilogue before them
+        const int s_mid = ck > 0 ? min(s0 + D, s1) : s0;
+        for (int s = s0; s < s1; ++s)
+            step(s, s < s_mid);
+
+        // ---- epilogue: bias, GELU, one rounding; each wave transposes one
+        // 64 x 32 tile at a time through its own 4 KB of LDS, then stores 16
+        // bytes per lane, 64 contiguous bytes per row: exactly NSTORE store
+        // instructions per wave.
+        const int h = lane >> 5;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int64_t n_tile = (int64_t)(g * G + wh * 4 + j) * TILE;
+            uint32_t bw[16];
+#pragma unroll
+            for (int d = 0; d < 16; ++d)
+                bw[d] = 0u;
+            if (bias32) {
+                if (n_tile + TILE <= a.N) {
+#pragma unroll
+                    for (int d = 0; d < 16; ++d)
+                        bw[d] = bias32[n_tile / 2 + d];
+                } else if (n_tile < a.N) {  // ragged last tile row (N % 32 == 16)
+#pragma unroll
+                    for (int d = 0; d < 8; ++d)
+                        bw[d] = bias32[n_tile / 2 + d];
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < 2; ++u) {
+                const int r = u * 32 + (lane & 31);  // token row within the wave's 64
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t d0 = h ? bw[4 * q + 2] : bw[4 * q];
+                    const uint32_t d1 = h ? bw[4 * q + 3] : bw[4 * q + 1];
+                    float v[4] = {acc[u][j][4 * q] + E::to_f32(d0 & 0xffff),
+                                  acc[u][j][4 * q + 1] + E::to_f32(d0 >> 16),
+                                  acc[u][j][4 * q + 2] + E::to_f32(d1 & 0xffff),
+                                  acc[u][j][4 * q + 3] + E::to_f32(d1 >> 16)};
+                    if (GELU) {
+#pragma unroll
+                        for (int x = 0; x < 4; ++x)
+                            v[x] = gelu_erf(v[x]);
                     }
                     uint2 o;
                     o.x = (uint32_t)E::from_f32(v[0]) | ((uint32_t)E::from_f32(v[1]) << 16);
                     o.y = (uint32_t)E::from_f32(v[2]) | ((uint32_t)E::from_f32(v[3]) << 16);
-                    const int row = t * 32 + (lane & 31);
-                    eb2[row * (EROW * 2) + (jj * 32 + n_off) / 4] = o;
+                    // row r, outputs 8q + 4h .. + 3: 16-byte chunk q ^ eswz(r), half h
+                    lds_write8(ebase + r * 64 + ((q ^ eswz(r)) * 16) + h * 8, o);
                 }
             }
-        }
-        __syncthreads();
-        const bool second = jp + 1 < rows_valid;
+            v4i ov[4];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            const int row = i * 8 + (lane >> 3), ch = lane & 7;
-            const int64_t m = m0 + wave * 64 + row;
-            const int64_t n = (int64_t)(row0 + jp) * TILE + ch * 8;
-            if (m < a.M && n < a.N && (ch < 4 || second))
-                *(uint4*)(a.Y + (m * a.ldy + n) * 2) = eb[row * EROW + ch];
+            for (int i = 0; i < 4; ++i) {
+                const int r = i * 16 + (lane >> 2), c = lane & 3;
+                ov[i] = lds_read16<0>(ebase + r * 64 + ((c ^ eswz(r)) * 16));
+            }
+            lds_wait();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                after_wait(ov[i]);
+                const int r = i * 16 + (lane >> 2), c = lane & 3;
+                const int64_t m = (int64_t)mt * BM + wm * 64 + r;
+                const int64_t n = n_tile + c * 8;
+                uint4* dst = (m < a.M && n < a.N) ? (uint4*)(Y + (m * a.ldy + n) * 2) : &g_sink[lane];
+                *dst = __builtin_bit_cast(uint4, ov[i]);
+            }
         }
-        __syncthreads();
     }
+    // no DMA may still be writing this workgroup's LDS when it ends
+    __builtin_amdgcn_s_waitcnt(0);
 }
 
 // fp32: 64 tokens x 16 outputs per workgroup; thread = one token x 4 outputs.
@@ -310,41 +499,70 @@ __global__ __launch_bounds__(256) void k_linear_f32(const float* __restrict__ X,
     }
 }
 
-inline unsigned grid_items(int64_t n_items) { return (unsigned)(((n_items + 7) / 8) * 8); }
+inline int num_cus()
+{
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        n = 256;
+    return n;
+}
 
 template <bool DENSE>
 hipError_t launch16(int dtype, bool gelu, const Args& a, hipStream_t s)
 {
-    const dim3 grid(grid_items((int64_t)a.n_mtiles * a.n_groups)), block(NT);
+    if (a.d.n_items <= 0)
+        return hipSuccess;
+    int P = num_cus() & ~7;
+    const int need = (a.d.n_items + 7) / 8 * 8;
+    if (P < 8)
+        P = 8;
+    if (P > need)
+        P = need;
+    const dim3 grid(P), block(NT);
+    const bool ktail = (a.d.K % TILE) != 0;
+#define LPV_LAUNCH1(DT_, GELU_, KT_)                                                              \
+    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_>), grid, block, 0, s, a.d, a.X,         \
+                       a.stream, a.step_ptr, a.step_meta, a.group_order, a.W,                     \
+                       (const uint32_t*)a.bias, a.Y)
+#define LPV_LAUNCH(DT_, GELU_)                                                                    \
+    do {                                                                                          \
+        if (ktail)                                                                                \
+            LPV_LAUNCH1(DT_, GELU_, true);                                                        \
+        else                                                                                      \
+            LPV_LAUNCH1(DT_, GELU_, false);                                                       \
+    } while (0)
     if (dtype == LPV_BF16) {
         if (gelu)
-            hipLaunchKernelGGL((k_linear16<LPV_BF16, true, DENSE>), grid, block, 0, s, a);
+            LPV_LAUNCH(LPV_BF16, true);
         else
-            hipLaunchKernelGGL((k_linear16<LPV_BF16, false, DENSE>), grid, block, 0, s, a);
+            LPV_LAUNCH(LPV_BF16, false);
     } else {
         if (gelu)
-            hipLaunchKernelGGL((k_linear16<LPV_F16, true, DENSE>), grid, block, 0, s, a);
+            LPV_LAUNCH(LPV_F16, true);
         else
-            hipLaunchKernelGGL((k_linear16<LPV_F16, false, DENSE>), grid, block, 0, s, a);
+            LPV_LAUNCH(LPV_F16, false);
     }
+#undef LPV_LAUNCH
+#undef LPV_LAUNCH1
     return hipGetLastError();
 }
 
 Args base_args(const LinearCall& c, int64_t N, int64_t K)
 {
     Args a = {};
+    a.d.ldx = c.ldx;
+    a.d.M = c.M;
+    a.d.K = K;
+    a.d.N = N;
+    a.d.ldy = c.ldy;
+    a.d.n_tile_rows = (int32_t)((N + TILE - 1) / TILE);
+    a.d.n_tile_cols = (int32_t)((K + TILE - 1) / TILE);
+    a.d.n_groups = (a.d.n_tile_rows + G - 1) / G;
+    a.d.n_items = (int32_t)((c.M + BM - 1) / BM) * a.d.n_groups;
     a.X = (const char*)c.X;
-    a.ldx = c.ldx;
-    a.M = c.M;
-    a.K = K;
-    a.N = N;
     a.bias = (const char*)c.bias;
     a.Y = (char*)c.Y;
-    a.ldy = c.ldy;
-    a.n_tile_rows = (int32_t)((N + TILE - 1) / TILE);
-    a.n_tile_cols = (int32_t)((K + TILE - 1) / TILE);
-    a.n_groups = (a.n_tile_rows + G - 1) / G;
-    a.n_mtiles = (int32_t)((c.M + BM - 1) / BM);
     return a;
 }
 
@@ -377,9 +595,7 @@ hipError_t launch_bsr_linear(const lpv_bsr* h, const LinearCall& c, hipStream_t 
     Args a = base_args(c, h->N, h->K);
     a.stream = (const uint4*)h->stream_vals;
     a.step_ptr = h->step_ptr;
-    a.step_col = h->step_col;
-    a.step_bits = h->step_bits;
-    a.step_tile = h->step_tile;
+    a.step_meta = h->step_meta;
     a.group_order = h->group_order;
     return launch16<false>(h->dtype, c.gelu != 0, a, s);
 }
@@ -392,7 +608,7 @@ hipError_t launch_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K,
                                 (const float*)W, ldw, (const float*)c.bias, (float*)c.Y, c.ldy, s);
     Args a = base_args(c, N, K);
     a.W = (const char*)W;
-    a.ldw = ldw;
+    a.d.ldw = ldw;
     return launch16<true>(dtype, c.gelu != 0, a, s);
 }
 

@@ -13,7 +13,7 @@ namespace lpv {
 // one pair of 32x32x16 matrix-core instructions.
 constexpr int TILE = 32;
 // Tile rows per group: a workgroup owns one token tile times one group.
-constexpr int GROUP_TILES = 4;
+constexpr int GROUP_TILES = 8;
 // Tokens per workgroup.
 constexpr int BM = 256;
 
@@ -43,6 +43,7 @@ struct lpv_bsr {
     int32_t* step_col;     // n_steps
     int32_t* step_bits;    // n_steps
     int32_t* step_tile;    // n_steps
+    int2* step_meta;       // n_steps: {col | bits << 16, tile}, what the linear kernel reads
     void* stream_vals;     // n_tiles * TILE * TILE elements, operand order
 };
 

@@ -203,7 +203,8 @@ __global__ __launch_bounds__(64) void k_sched_fill(PackArgs a, const int32_t* __
                                                    const int32_t* __restrict__ group_tile0,
                                                    int32_t* __restrict__ step_col,
                                                    int32_t* __restrict__ step_bits,
-                                                   int32_t* __restrict__ step_tile)
+                                                   int32_t* __restrict__ step_tile,
+                                                   int2* __restrict__ step_meta)
 {
     const int g = blockIdx.x;
     int s = step_ptr[g], t = group_tile0[g];
@@ -218,6 +219,7 @@ __global__ __launch_bounds__(64) void k_sched_fill(PackArgs a, const int32_t* __
             step_col[pos] = tc;
             step_bits[pos] = bits;
             step_tile[pos] = t + inc - pc;
+            step_meta[pos] = make_int2(tc | (bits << 16), t + inc - pc);
         }
         s += __popcll(b);
         t += __shfl(inc, 63, 64);
@@ -319,7 +321,8 @@ hipError_t launch_pack_fill(const PackArgs& a, const lpv_bsr* h, hipStream_t s)
         return e;
     if (a.n_groups > 0)
         hipLaunchKernelGGL(k_sched_fill, dim3(a.n_groups), dim3(64), 0, s, a, h->step_ptr,
-                           h->group_tile0, h->step_col, h->step_bits, h->step_tile);
+                           h->group_tile0, h->step_col, h->step_bits, h->step_tile,
+                           h->step_meta);
     if (h->n_steps > 0)
         hipLaunchKernelGGL(k_stream_fill, dim3((unsigned)h->n_steps), dim3(256), 0, s, a,
                            h->step_ptr, h->step_col, h->step_bits, h->step_tile,
