@@ -59,6 +59,50 @@ def algorithmic_bytes(M, N, K, nnzb, b_r, b_c, kused_cols, es=2):
     return es * (M * kused_cols + M * N + nnzb * b_r * b_c + N) + 4 * (N // b_r + 1 + nnzb)
 
 
+SPARSE_KERNEL = "k_linear16<2, false, false"   # bf16, no GELU, block-sparse (demangled prefix)
+CALIB_BYTES = 1 << 30                        # the calibration copy reads and writes this much
+
+
+def write_traffic(fetch_csv, write_csv, command):
+    """HBM bytes per launch of the block-sparse kernel from two rocprofv3
+    counter runs of ``--profile-pass`` (FETCH_SIZE, then WRITE_SIZE, KiB per
+    dispatch), each scaled by what the same counter reads for the 1 GiB
+    device-to-device copy of that pass; written next to the other profiles."""
+    import csv
+
+    def per_dispatch(path, counter):
+        rows = [r for r in csv.DictReader(open(path)) if r["Counter_Name"] == counter]
+        kern = [float(r["Counter_Value"]) for r in rows if SPARSE_KERNEL in r["Kernel_Name"]]
+        copies = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not kern or not copies:
+            raise SystemExit("%s: no %s rows for the kernel or the copy" % (path, counter))
+        return sum(kern) / len(kern), max(copies)
+
+    fk, fc = per_dispatch(fetch_csv, "FETCH_SIZE")
+    wk, wc = per_dispatch(write_csv, "WRITE_SIZE")
+    f_scale = CALIB_BYTES / (fc * 1024.0)
+    w_scale = CALIB_BYTES / (wc * 1024.0)
+    out = {"kernel": "k_linear16 (lpv_bsr_linear), bf16, no GELU",
+           "workload": "DeiT-B fc1 batch 256, 32x32 blocks, 50% block sparsity",
+           "kernel_source_sha256_16": kernel_source_hash(),
+           "fetch_kib_per_dispatch": round(fk, 1), "write_kib_per_dispatch": round(wk, 1),
+           "copy_1GiB_fetch_kib": round(fc, 1), "copy_1GiB_write_kib": round(wc, 1),
+           "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+           "hbm_read_bytes_per_launch": int(fk * 1024 * f_scale),
+           "hbm_write_bytes_per_launch": int(wk * 1024 * w_scale),
+           "hbm_bytes_per_launch": int(fk * 1024 * f_scale + wk * 1024 * w_scale),
+           "counter_runs": [
+               "rocprofv3 --pmc FETCH_SIZE -d gpurun_out/pmc_fetch -o fetch --output-format csv "
+               "-- python bench.py --profile-pass",
+               "rocprofv3 --pmc WRITE_SIZE -d gpurun_out/pmc_write -o write --output-format csv "
+               "-- python bench.py --profile-pass"],
+           "command": command}
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out, indent=1))
+
+
 def time_launches(fn, steps, warmup):
     import torch
     for _ in range(warmup):
@@ -98,10 +142,18 @@ def cpu_baseline(w, target_s=12.0):
         if t >= target_s / 4 or rows >= w.M:
             break
         rows = min(w.M, int(rows * max(2.0, target_s / 4 / max(t, 1e-3))))
+    reps, total = 1, t
+    while rows >= w.M and total < target_s and reps < 10:  # the whole workload: repeat it
+        X = w.X[:rows]
+        t0 = time.perf_counter()
+        oracle.linear(X, w.W, w.dtype, w.b_r, w.b_c, w.mask, w.bias, gelu=w.gelu, nthreads=nt)
+        total += time.perf_counter() - t0
+        reps += 1
+    t = total / reps
     flops = w.kept_flops(rows)
     return {"value": flops / t / 1e12, "unit": "TFLOP/s", "cores": nt, "kind": "oracle",
             "sample": "first %d of %d token rows of the same workload (float64 mask expansion + "
-                      "triple loop), %.1f s" % (rows, w.M, t)}
+                      "triple loop), mean of %d runs, %.1f s each" % (rows, w.M, reps, t)}
 
 
 def main():
@@ -114,7 +166,15 @@ def main():
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f16"])
     ap.add_argument("--block", type=int, default=32)
     ap.add_argument("--sparsity", type=int, default=50)
+    ap.add_argument("--profile-pass", action="store_true",
+                    help="only 3 launches of each path and a 1 GiB device copy (rocprofv3 counter runs)")
+    ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="turn two --profile-pass counter CSVs into the HBM traffic summary")
     args = ap.parse_args()
+
+    if args.write_traffic:
+        write_traffic(*args.write_traffic, command=" ".join(["python bench.py"] + sys.argv[1:]))
+        return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the block-sparse layer shards over tokens with no "
@@ -154,6 +214,18 @@ def main():
 
     sparse = lambda: lpv.bsr_linear(h, X, b, Y, epi=epi)
     dense = lambda: lpv.dense_linear(W, X, b, Yd, epi=epi)
+    if args.profile_pass:
+        for _ in range(3):
+            sparse()
+        for _ in range(3):
+            dense()
+        src = torch.empty(CALIB_BYTES // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("profile pass done")
+        h.close()
+        return
     wall, ms = time_launches(sparse, args.steps, args.warmup)
     dwall, dms = time_launches(dense, args.steps, args.warmup)
     # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
