@@ -49,7 +49,7 @@ constexpr int SLOT = XU4 + WU4;     // one ring slot: 32 KB
 constexpr int NSTORE = 16;          // store instructions per wave per item
 constexpr int EPI_U4 = 64 * 4;      // per-wave epilogue tile: 64 rows x 64 bytes
 constexpr int LPS = 4;              // DMA instructions per wave per step (2 X + 2 W)
-constexpr int WAIT_A = LPS * (D - 1);        // DMA still allowed in flight at a step
+constexpr int WAIT_A = LPS * (D - 2);        // DMA still allowed in flight at a step's barrier
 constexpr int WAIT_B = WAIT_A + NSTORE;      // ... when an item's stores were issued since
 
 static_assert(XU4 == 2 * 8 * 64 && WU4 == 2 * 8 * 64, "2 X and 2 W DMA instructions per wave");
@@ -238,43 +238,57 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             }
         }
     };
-    // `meta` is step_meta[ps], loaded by the caller ahead of time (sparse only)
-    auto produce = [&](int slot, int2 meta) {
-        const uint4* xdst = smem + slot * SLOT + wave * 128;
-        const uint4* wdst = smem + slot * SLOT + XU4 + wave * 128;
+    // The DMA of one step: sources and LDS destinations of this wave's 4
+    // instructions.  `meta` is step_meta[ps], loaded by the caller ahead of
+    // time (sparse only).
+    struct Dma {
+        const char* src[4];
+        uint4* dst[4];
+    };
+    auto dma_prep = [&](int slot, int2 meta, Dma& d) {
+        uint4* xdst = smem + slot * SLOT + wave * 128;
+        uint4* wdst = smem + slot * SLOT + XU4 + wave * 128;
+        d.dst[0] = xdst;
+        d.dst[1] = xdst + 64;
+        d.dst[2] = wdst;
+        d.dst[3] = wdst + 64;
         if (pk < my_items) {
             const int col = DENSE ? ps : (meta.x & 0xffff);
             const int64_t coff = (int64_t)col * TILE * 2;  // bytes to column tile col
-            const char* xs0 = xsrc[0] + coff;
-            const char* xs1 = xsrc[1] + coff;
-            const char *ws0, *ws1;
+            d.src[0] = xsrc[0] + coff;
+            d.src[1] = xsrc[1] + coff;
             if (DENSE) {
-                ws0 = wsrc[0] + coff;
-                ws1 = wsrc[1] + coff;
+                d.src[2] = wsrc[0] + coff;
+                d.src[3] = wsrc[1] + coff;
             } else {
                 const char* tiles = (const char*)stream + (int64_t)meta.y * 2048 + wave * 2048;
-                ws0 = tiles + lane * 16;
-                ws1 = tiles + 1024 + lane * 16;
+                d.src[2] = tiles + lane * 16;
+                d.src[3] = tiles + 1024 + lane * 16;
             }
             if (KTAIL && col == last_col) {  // columns past K read the zero line
-                if (col * TILE + xcol[0] >= a.K) xs0 = zero;
-                if (col * TILE + xcol[1] >= a.K) xs1 = zero;
-                if (DENSE && col * TILE + wcol[0] >= a.K) ws0 = zero;
-                if (DENSE && col * TILE + wcol[1] >= a.K) ws1 = zero;
+                if (col * TILE + xcol[0] >= a.K) d.src[0] = zero;
+                if (col * TILE + xcol[1] >= a.K) d.src[1] = zero;
+                if (DENSE && col * TILE + wcol[0] >= a.K) d.src[2] = zero;
+                if (DENSE && col * TILE + wcol[1] >= a.K) d.src[3] = zero;
             }
-            dma16(xs0, (uint4*)xdst);
-            dma16(xs1, (uint4*)xdst + 64);
-            dma16(ws0, (uint4*)wdst);
-            dma16(ws1, (uint4*)wdst + 64);
-            if (++ps >= ps_end)
-                next_item();
         } else {
             // past the last step: the same instruction count, into a free slot
-            dma16(zero, (uint4*)xdst);
-            dma16(zero, (uint4*)xdst + 64);
-            dma16(zero, (uint4*)wdst);
-            dma16(zero, (uint4*)wdst + 64);
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                d.src[i] = zero;
         }
+    };
+    auto dma_advance = [&]() {
+        if (pk < my_items && ++ps >= ps_end)
+            next_item();
+    };
+    auto produce = [&](int slot, int2 meta) {
+        Dma d;
+        dma_prep(slot, meta, d);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            dma16(d.src[i], d.dst[i]);
+        dma_advance();
     };
 
     next_item();
@@ -299,8 +313,13 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     const uint32_t wa_addr = smem0 + XU4 * 16 + lane * 16;
     const uint32_t ebase = smem0 + NS * SLOT * 16 + wave * (EPI_U4 * 16);
 
+    // Step 0 has landed everywhere before anyone reads it.
+    wait_vm_lgkm0<LPS * (D - 1)>();
+    barrier_step();
+
     f32x16 acc[2][4];
-    int t = 0;  // steps consumed
+    int t = 0;     // steps consumed
+    int e = -16;   // last step of the last item written out
     for (int ck = 0; ck < my_items; ++ck) {
         int g, mt, s0, s1;
         group_of(ck, g, mt);
@@ -314,53 +333,68 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                 for (int v = 0; v < 16; ++v)
                     acc[u][j][v] = 0.0f;
 
-        // one step: wait for its DMA, let the producer refill the freed slot,
-        // then LDS -> matrix cores.  During an item's first D steps the
-        // previous epilogue's NSTORE stores may still be in flight too.  The
-        // metadata of the next step (the consumer's bits, the producer's column
-        // and tile) is loaded a step ahead, so its latency hides behind the
-        // matrix cores.
+        // One step.  The two waves of a SIMD take turns: group A (row half 0)
+        // reads its operands after the step's barrier and then runs the matrix
+        // cores; group B (row half 1) reads before the barrier and computes
+        // after it, so one wave's LDS reads overlap the other's MFMAs.  Before
+        // the barrier of step u every wave has waited for its DMA of step
+        // u + 1 (group B reads that step before the next barrier); after it,
+        // the slot of step u - 1 is free and is refilled with step u + D.  The
+        // wait also covers an epilogue's stores when one was issued after that
+        // DMA.  Metadata of the next step is loaded a step ahead.
         int bits = DENSE ? rows : (s0 < s1 ? (step_meta[s0].x >> 16) : 0);
-        auto step = [&](int s, bool after_epilogue) {
-            if (after_epilogue)
-                wait_vm_lgkm0<WAIT_B>();
-            else
-                wait_vm_lgkm0<WAIT_A>();
-            barrier_step();
-            produce((t + D) & (NS - 1), pmeta);
-            if (!DENSE) {
-                pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
-            }
+        auto step = [&](int s) {
             const int cur = bits;
             if (!DENSE)
                 bits = s + 1 < s1 ? (step_meta[s + 1].x >> 16) : 0;
-
             const uint32_t slot_off = (uint32_t)(t & (NS - 1)) * (SLOT * 16);
-            // all of this step's operand reads first, one wait, then the matrix cores
-            v4i xa[2][2], wf[4][2];
-#pragma unroll
-            for (int ks = 0; ks < 2; ++ks) {
-                xa[0][ks] = lds_read16<0>(xa_addr[ks] + slot_off);
-                xa[1][ks] = lds_read16<2048>(xa_addr[ks] + slot_off);
-            }
             const int bh = (cur >> (4 * wh)) & 15;
-            uint32_t wa = wa_addr + slot_off + (wh ? __popc(cur & 15) * 2048 : 0);
+            v4i xa[2][2], wf[4][2];
+            auto read_ops = [&]() {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                if (bh & (1 << j)) {
-                    wf[j][0] = lds_read16<0>(wa);
-                    wf[j][1] = lds_read16<1024>(wa);
-                    wa += 2048;
+                for (int ks = 0; ks < 2; ++ks) {
+                    xa[0][ks] = lds_read16<0>(xa_addr[ks] + slot_off);
+                    xa[1][ks] = lds_read16<2048>(xa_addr[ks] + slot_off);
                 }
+                uint32_t wa = wa_addr + slot_off + (wh ? __popc(cur & 15) * 2048 : 0);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if (bh & (1 << j)) {
+                        wf[j][0] = lds_read16<0>(wa);
+                        wf[j][1] = lds_read16<1024>(wa);
+                        wa += 2048;
+                    }
+                }
+            };
+            auto sync = [&]() {
+                if (e >= t - 2)
+                    wait_vm_lgkm0<WAIT_B>();
+                else
+                    wait_vm_lgkm0<WAIT_A>();
+                barrier_step();
+            };
+            Dma dm;
+            if (wh == 0) {
+                sync();
+                read_ops();
+                dma_prep((t + D) & (NS - 1), pmeta, dm);
+                lds_wait();
+            } else {
+                read_ops();
+                lds_wait();
+                sync();
+                dma_prep((t + D) & (NS - 1), pmeta, dm);
             }
-            lds_wait();
 #pragma unroll
             for (int u = 0; u < 2; ++u)
 #pragma unroll
                 for (int ks = 0; ks < 2; ++ks)
                     after_wait(xa[u][ks]);
+            // the refill of the freed slot goes out one instruction at a time
+            // between the matrix-core instructions
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
+                dma16(dm.src[j], dm.dst[j]);
                 if (bh & (1 << j)) {
                     after_wait(wf[j][0]);
                     after_wait(wf[j][1]);
@@ -372,18 +406,20 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                     acc[1][j] = E::mma(w1, __builtin_bit_cast(F, xa[1][1]), acc[1][j]);
                 }
             }
+            dma_advance();
+            if (!DENSE)
+                pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
             ++t;
         };
-        // the first D steps of every item but the first wait past the stores of
-        // the epilogue before them
-        const int s_mid = ck > 0 ? min(s0 + D, s1) : s0;
         for (int s = s0; s < s1; ++s)
-            step(s, s < s_mid);
+            step(s);
+        e = t - 1;
 
         // ---- epilogue: bias, GELU, one rounding; each wave transposes one
         // 64 x 32 tile at a time through its own 4 KB of LDS, then stores 16
         // bytes per lane, 64 contiguous bytes per row: exactly NSTORE store
-        // instructions per wave.
+        // instructions per wave.  The stores are non-temporal: Y is not read
+        // again, and keeping it out of L2 leaves L2 to X and the tile stream.
         const int h = lane >> 5;
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -440,7 +476,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                 const int64_t m = (int64_t)mt * BM + wm * 64 + r;
                 const int64_t n = n_tile + c * 8;
                 uint4* dst = (m < a.M && n < a.N) ? (uint4*)(Y + (m * a.ldy + n) * 2) : &g_sink[lane];
-                *dst = __builtin_bit_cast(uint4, ov[i]);
+                __builtin_nontemporal_store(ov[i], (v4i*)dst);
             }
         }
     }
