@@ -147,14 +147,17 @@ lpv_status lpv_bsr_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, void* stre
 /*
  * lpv_bsr_linear -- Y = g(X * W~^T + b), the block-sparse hot path.
  *
- * X     device, M x K, row stride ldx >= K.
+ * X     device, M x K, row stride K <= ldx <= 2^22 (the kernels address a
+ *       256-token slice of X with 32-bit byte offsets).
  * bias  device, N elements, or NULL for no bias.
  * Y     device, M x N, row stride ldy >= N; must not overlap X.
  * epi   LPV_EPI_NONE or LPV_EPI_GELU (exact-erf GELU after the bias).
  *
  * Each token tile times each group of output tile rows walks only the kept
  * tiles of its rows, on the matrix cores for bf16/fp16.  M = 0 is a no-op.
- * One kernel launch, no allocation, no host synchronisation.
+ * One kernel launch per run of output groups whose per-launch tables fit in
+ * LDS (a single launch for ViT-sized layers), no allocation, no host
+ * synchronisation.
  * Errors: INVALID_ARG, SHAPE, ALIAS, HIP.
  */
 lpv_status lpv_bsr_linear(const lpv_bsr* h, const void* X, int64_t ldx, int64_t M,
@@ -162,10 +165,10 @@ lpv_status lpv_bsr_linear(const lpv_bsr* h, const void* X, int64_t ldx, int64_t 
                           void* stream);
 
 /*
- * lpv_dense_linear -- Y = g(X * W^T + b) with a dense W (N x K, row stride ldw),
- * through the library's own matrix-core kernel: the reference point for the
- * speed-up of the block-sparse path.  Same conventions as lpv_bsr_linear;
- * N and K must be multiples of 16.
+ * lpv_dense_linear -- Y = g(X * W^T + b) with a dense W (N x K, row stride
+ * K <= ldw <= 2^22), through the library's own matrix-core kernel: the
+ * reference point for the speed-up of the block-sparse path.  Same
+ * conventions as lpv_bsr_linear; N and K must be multiples of 16.
  */
 lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
                             const void* X, int64_t ldx, int64_t M, const void* bias, void* Y,

@@ -43,6 +43,9 @@ int elem_size(int dt)
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 constexpr int64_t MAX_DIM = 65536;  // N and K (schedule tables are sized for it)
+// Leading dimensions of X and W: the kernels address a 256-row tile of either
+// with 32-bit byte offsets.
+constexpr int64_t MAX_LD = (int64_t)1 << 22;
 constexpr int64_t MAX_M = (int64_t)1 << 31;
 
 // Device allocations fail on purpose when LPV_FAULT_INJECT=alloc (tests of
@@ -78,6 +81,9 @@ lpv_status check_linear(int es, int64_t N, int64_t K, const void* X, int64_t ldx
         return fail(LPV_ERR_INVALID_ARG, "unknown epilogue %d", epi);
     if (ldx < K)
         return fail(LPV_ERR_INVALID_ARG, "ldx = %lld < K = %lld", (long long)ldx, (long long)K);
+    if (ldx > MAX_LD)
+        return fail(LPV_ERR_INVALID_ARG, "ldx = %lld is above %lld", (long long)ldx,
+                    (long long)MAX_LD);
     if (ldy < N)
         return fail(LPV_ERR_INVALID_ARG, "ldy = %lld < N = %lld", (long long)ldy, (long long)N);
     if ((ldx * es) % 16 || (ldy * es) % 16)
@@ -100,10 +106,11 @@ void free_handle(lpv_bsr* h)
     if (!h)
         return;
     void* bufs[] = {h->meta, h->col_idx, h->values, h->step_col, h->step_bits, h->step_tile,
-                    h->step_meta, h->stream_vals};
+                    h->walk, h->stream_vals};
     for (void* p : bufs)
         if (p)
             (void)hipFree(p);
+    delete[] h->gdesc_host;
     delete h;
 }
 
@@ -168,8 +175,10 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
     h->n_groups = (h->n_tile_rows + lpv::GROUP_TILES - 1) / lpv::GROUP_TILES;
     hipStream_t s = (hipStream_t)stream;
 
-    // one buffer for row_ptr, group_order, step_ptr, group_tile0 and the plan
-    const size_t n_meta = (size_t)(h->R + 1) + 3 * (size_t)(h->n_groups + 1) + 4;
+    // one buffer for gdesc (16-byte entries first), row_ptr, group_order,
+    // step_ptr, group_tile0 and the plan
+    const size_t n_meta = 4 * (size_t)h->n_groups + (size_t)(h->R + 1) +
+                          3 * (size_t)(h->n_groups + 1) + 4;
     void* meta = nullptr;
     hipError_t e = dmalloc(&meta, n_meta * sizeof(int32_t));
     if (e != hipSuccess) {
@@ -183,7 +192,8 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
         free_handle(h);
         return hip_fail(e, "hipGetDevice");
     }
-    h->row_ptr = (int32_t*)meta;
+    h->gdesc = (int4*)meta;
+    h->row_ptr = (int32_t*)(h->gdesc + h->n_groups);
     h->group_order = h->row_ptr + (h->R + 1);
     h->step_ptr = h->group_order + (h->n_groups + 1);
     h->group_tile0 = h->step_ptr + (h->n_groups + 1);
@@ -205,9 +215,21 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
     a.n_groups = h->n_groups;
 
     lpv::Plan plan = {};
-    e = lpv::launch_pack_plan(a, h->row_ptr, h->step_ptr, h->group_tile0, h->group_order, plan_d, s);
+    const bool mfma_path = dt != LPV_F32;
+    if (mfma_path) {
+        h->gdesc_host = new (std::nothrow) int4[h->n_groups];
+        if (!h->gdesc_host) {
+            free_handle(h);
+            return fail(LPV_ERR_ALLOC, "host allocation failed");
+        }
+    }
+    e = lpv::launch_pack_plan(a, h->row_ptr, h->step_ptr, h->group_tile0, h->group_order,
+                              h->gdesc, plan_d, s);
     if (e == hipSuccess)
         e = hipMemcpyAsync(&plan, plan_d, sizeof plan, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess && mfma_path)
+        e = hipMemcpyAsync(h->gdesc_host, h->gdesc, (size_t)h->n_groups * sizeof(int4),
+                           hipMemcpyDeviceToHost, s);
     if (e == hipSuccess)
         e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
@@ -215,9 +237,9 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
         return hip_fail(e, "pack plan");
     }
     h->nnzb = plan.nnzb;
-    const bool mfma_path = dt != LPV_F32;
     h->n_steps = mfma_path ? plan.n_steps : 0;
     h->n_tiles = mfma_path ? plan.n_tiles : 0;
+    h->n_walk = mfma_path ? plan.n_walk : 0;
 
     const size_t blk = (size_t)b_r * b_c * es;
     e = dmalloc((void**)&h->col_idx, (size_t)h->nnzb * sizeof(int32_t));
@@ -230,14 +252,9 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
         if (e == hipSuccess)
             e = dmalloc((void**)&h->step_tile, (size_t)h->n_steps * sizeof(int32_t));
         if (e == hipSuccess)
-            e = dmalloc((void**)&h->step_meta, (size_t)h->n_steps * sizeof(int2));
+            e = dmalloc((void**)&h->walk, (size_t)h->n_walk * sizeof(int2));
         if (e == hipSuccess)
-            e = dmalloc(&h->stream_vals,
-                        (size_t)(h->n_tiles + lpv::GROUP_TILES) * lpv::TILE * lpv::TILE * es);
-        // the linear kernel's DMA reads up to GROUP_TILES tiles past a step's own
-        if (e == hipSuccess)
-            e = hipMemsetAsync((char*)h->stream_vals + (size_t)h->n_tiles * lpv::TILE * lpv::TILE * es,
-                               0, (size_t)lpv::GROUP_TILES * lpv::TILE * lpv::TILE * es, s);
+            e = dmalloc(&h->stream_vals, (size_t)h->n_tiles * lpv::TILE * lpv::TILE * es);
     }
     if (e != hipSuccess) {
         free_handle(h);
@@ -364,9 +381,9 @@ lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lp
     if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM || N % 16 || K % 16)
         return fail(LPV_ERR_SHAPE, "weight %lldx%lld: sides must be multiples of 16 in [16, %lld]",
                     (long long)N, (long long)K, (long long)MAX_DIM);
-    if (!W || ldw < K || (ldw * es) % 16 || !aligned16(W))
-        return fail(LPV_ERR_INVALID_ARG, "W must be non-NULL, 16-byte aligned, ldw >= K and a "
-                                         "multiple of 16 bytes");
+    if (!W || ldw < K || ldw > MAX_LD || (ldw * es) % 16 || !aligned16(W))
+        return fail(LPV_ERR_INVALID_ARG, "W must be non-NULL, 16-byte aligned, K <= ldw <= 2^22 "
+                                         "and ldw a multiple of 16 bytes");
     lpv_status st = check_linear(es, N, K, X, ldx, M, bias, Y, ldy, epi);
     if (st != LPV_OK || M == 0)
         return st;

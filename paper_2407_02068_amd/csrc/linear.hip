@@ -6,33 +6,45 @@
 // An item walks its group's steps -- the 32-wide reduction columns where any
 // of its rows keeps a tile; other columns are never touched -- so its work is
 // proportional to the kept tiles, the quantity the paper's cost model counts
-// (Sec. 3.4).
+// (Sec. 3.4).  The walk starts at a per-group column and wraps around, so the
+// groups that work on one token tile at the same time read different X
+// columns.
 //
 // One persistent workgroup of 8 waves per compute unit takes items in turn
 // (consecutive items, which share a token tile, go to workgroups on the same
 // XCD so the X slice is fetched from HBM once per XCD L2).  Its steps, across
 // item boundaries, flow through a 4-slot LDS ring:
 //   - gfx950 global->LDS DMA (global_load_lds_dwordx4) stages each step's X
-//     slice [256 tokens x 32 columns] and kept W tiles, 3 steps ahead, with
-//     16-byte coalesced loads and no registers in between; every wave issues
-//     the same number of DMA instructions per step (rows or tiles past the
-//     operands read a zero line), so a fixed vmcnt wait tells a wave that its
-//     part of a step has landed, and one barrier per step tells everyone;
+//     slice [256 tokens x 32 columns] (two instructions per wave) and the
+//     step's kept W tiles (tile j by wave j, two instructions), 3 steps ahead,
+//     16 bytes per lane with no registers in between;
+//   - a wave's DMA count per step is 2 or 4, known from the step's row bits,
+//     which travel from the producer cursor to the consumer in a 64-bit queue
+//     (16 bits per step in flight); the wait before each step's barrier
+//     leaves exactly the later steps' DMA (and a finished item's stores) in
+//     flight, and the barrier tells every wave that the whole step landed;
 //   - wave (m, h) takes tokens [64m, 64m + 64) and tile rows [4h, 4h + 4) of
 //     the group and issues v_mfma_f32_32x32x16 (bf16 / fp16 in, float32
 //     accumulate) for each kept tile; the two waves of a SIMD cover both row
-//     halves, so every SIMD gets the step's whole kept count.
-// The epilogue adds the bias (scalar loads), applies GELU if asked, rounds once
-// to the element type and stores Y straight from the accumulators, while the
-// DMA of the next item's first steps is already in flight.
+//     halves, so every SIMD gets the step's whole kept count.  The h = 1 wave
+//     reads its operands before the barrier and the h = 0 wave after it, so
+//     one wave's LDS reads overlap the other's matrix-core work.
+// The step loop carries no division and no scalar load on its critical path:
+// the per-group descriptors (group, first step, step count, first column
+// walked) are built at pack time, item coordinates advance by constants, and
+// the next step's metadata is loaded one step ahead.
+// The epilogue adds the bias, applies GELU if asked, rounds once to the element
+// type and stores Y (16 bytes per lane, transposed through LDS), while the DMA
+// of the next item's first steps is already in flight.
 //
 // MFMA operand roles: A = a W tile (rows = output features), B = X slice
 // transposed (columns = tokens), so D[n][token]: lane l holds token l % 32 and,
 // per group of 4 accumulator registers, 4 consecutive output features.
 //
 // The dense path is the same kernel with every tile kept and W read straight
-// from its row-major layout.  fp32 runs a plain VALU kernel over the canonical
-// BSR arrays (it serves the small fp32 configuration only).
+// from its row-major layout into the same slice layout as X.  fp32 runs a plain
+// VALU kernel over the canonical BSR arrays (it serves the small fp32
+// configuration only).
 #include "lpv_device.h"
 #include "lpv_internal.h"
 
@@ -47,72 +59,93 @@ constexpr int XU4 = BM * 4;         // 16-byte chunks of one X slice (256 x 32 e
 constexpr int WU4 = G * 128;        // 16-byte chunks of G W tiles (32 x 32 elements each)
 constexpr int SLOT = XU4 + WU4;     // one ring slot: 32 KB
 constexpr int NSTORE = 16;          // store instructions per wave per item
-constexpr int EPI_U4 = 64 * 4;      // per-wave epilogue tile: 64 rows x 64 bytes
-constexpr int LPS = 4;              // DMA instructions per wave per step (2 X + 2 W)
-constexpr int WAIT_A = LPS * (D - 2);        // DMA still allowed in flight at a step's barrier
-constexpr int WAIT_B = WAIT_A + NSTORE;      // ... when an item's stores were issued since
+constexpr int TAB_U4 = 2048;        // per-call tables (walk, slot descriptors, bias): 32 KB
 
-static_assert(XU4 == 2 * 8 * 64 && WU4 == 2 * 8 * 64, "2 X and 2 W DMA instructions per wave");
-static_assert((NS * SLOT + 8 * EPI_U4) * 16 <= 163840, "LDS budget of one workgroup");
+static_assert(XU4 == 2 * 8 * 64 && WU4 == 2 * 8 * 64, "2 X and up to 2 W DMA instructions per wave");
+static_assert((NS * SLOT + TAB_U4) * 16 <= 163840, "LDS budget of one workgroup");
 
-// A zero line for DMA lanes outside X (token or column tails), and a sink for
-// store lanes outside Y: the instruction count of a wave never depends on
-// where the operands end.
+// A zero line for DMA lanes past K, and a sink for store lanes outside Y.
 static __device__ uint4 g_zero[1];
 static __device__ uint4 g_sink[64];
 
-// Sizes of one call (the arrays are separate __restrict__ kernel arguments,
-// so the schedule and bias reads can go through the scalar cache).
 struct Dims {
     int64_t ldx, M, K, N, ldw, ldy;
-    int32_t n_groups, n_tile_rows, n_tile_cols, n_items;
+    int32_t n_tile_rows, n_tile_cols, n_groups;
+    int32_t gs0, n_slots;   // this launch: launch slots [gs0, gs0 + n_slots) ...
+    int32_t n_items;        // ... times every token tile
+    int32_t p_div, p_mod;   // grid size divided by / modulo n_slots
+    int32_t walk0, n_walk;  // this launch's slice of the walk array
+    int32_t walk_off, bias_off;  // byte offsets of the walk and bias tables in LDS
 };
 
-struct Args {
-    Dims d;
-    const char* X;
-    const uint4* stream;       // sparse operand stream
-    const int32_t* step_ptr;
-    const int2* step_meta;
-    const int32_t* group_order;
-    const char* W;             // dense weight
-    const char* bias;
-    char* Y;
-};
+__device__ inline uint32_t lds_addr(const void* p)
+{
+    return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
 
-typedef __attribute__((address_space(3))) void* lds_ptr;
-
+// Global -> LDS DMA of 16 bytes per lane to 1 KB at a wave-uniform LDS base.
+// Issued from inline assembly: the compiler then neither drains this DMA
+// before every LDS read of the wave (as it must for the builtin, which it
+// knows writes LDS) nor counts it in its own vmcnt waits.  Every wait for it
+// is explicit (the ring protocol: vmcnt wait + barrier per step); the memory
+// clobber keeps the compiler's LDS reads in program order around it.
 __device__ inline void dma16(const void* src, uint4* lds_wave_base)
 {
-    __builtin_amdgcn_global_load_lds(src, (lds_ptr)lds_wave_base, 16, 0, 0);
+    asm volatile(
+        "s_nop 0\n"
+        "global_load_lds_dwordx4 %0, off"
+        :
+        : "v"(src), "{m0}"(lds_addr(lds_wave_base))
+        : "memory");
 }
 
-// s_waitcnt vmcnt(n) lgkmcnt(0) (gfx9 encoding; expcnt left alone)
-template <int N> __device__ inline void wait_vm_lgkm0()
+// The same from a wave-uniform base and a 32-bit per-lane byte offset (the
+// saddr + voffset form: no 64-bit address per lane is kept live).
+__device__ inline void dma16(const char* base, uint32_t off, uint4* lds_wave_base)
+{
+    asm volatile(
+        "s_nop 0\n"
+        "global_load_lds_dwordx4 %0, %1"
+        :
+        : "v"(off), "s"(base), "{m0}"(lds_addr(lds_wave_base))
+        : "memory");
+}
+
+// s_waitcnt vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt left alone)
+template <int N> __device__ inline void wait_vm()
 {
     static_assert(N < 64, "vmcnt is 6 bits");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (0 << 8) | ((N >> 4) << 14));
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-// The same with a wave-uniform count: s_waitcnt only takes an immediate, so
-// dispatch over the counts the ring can produce (larger ones wait for more,
-// which is always safe).
-__device__ inline void wait_vm_lgkm0_dyn(int n)
+// The wait before a step barrier and the barrier, as one small branch tree
+// (the compiler spends several times the instructions on it): case 0: nothing
+// of this wave's may stay in flight; 1: its last N DMA instructions may; 2:
+// its last NSTORE stores may; 3: both.
+template <int N> __device__ inline void step_barrier_wait(int cs)
 {
-#define LPV_W(N)                  \
-    case N:                       \
-        wait_vm_lgkm0<N>();       \
-        break;
-    switch (n) {
-        LPV_W(0) LPV_W(1) LPV_W(2) LPV_W(3) LPV_W(4) LPV_W(5) LPV_W(6) LPV_W(7) LPV_W(8)
-        LPV_W(9) LPV_W(10) LPV_W(11) LPV_W(12) LPV_W(13) LPV_W(14) LPV_W(15) LPV_W(16)
-        LPV_W(17) LPV_W(18) LPV_W(19) LPV_W(20) LPV_W(21) LPV_W(22) LPV_W(23) LPV_W(24)
-        LPV_W(25) LPV_W(26) LPV_W(27) LPV_W(28)
-    default:
-        wait_vm_lgkm0<28>();
-        break;
-    }
-#undef LPV_W
+    asm volatile(
+        "s_cmp_lt_u32 %0, 2\n"
+        "s_cbranch_scc1 1f\n"
+        "s_cmp_eq_u32 %0, 3\n"
+        "s_cbranch_scc0 2f\n"
+        "s_waitcnt vmcnt(%1)\n"
+        "s_branch 4f\n"
+        "2:\n"
+        "s_waitcnt vmcnt(%2)\n"
+        "s_branch 4f\n"
+        "1:\n"
+        "s_cmp_eq_u32 %0, 1\n"
+        "s_cbranch_scc0 3f\n"
+        "s_waitcnt vmcnt(%3)\n"
+        "s_branch 4f\n"
+        "3:\n"
+        "s_waitcnt vmcnt(0)\n"
+        "4:\n"
+        "s_barrier"
+        :
+        : "s"(cs), "i"(N + NSTORE), "i"(NSTORE), "i"(N)
+        : "memory", "scc");
 }
 
 __device__ inline void barrier_step()
@@ -122,365 +155,450 @@ __device__ inline void barrier_step()
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
-// 16-byte LDS read issued from inline assembly: the compiler then does not
-// treat it as a read of LDS that the in-flight DMA may be writing (it would
-// otherwise drain all DMA before every read).  The ring protocol (vmcnt wait +
-// barrier per step) is what orders these reads after the DMA that fills them,
-// and lds_wait() below after the reads themselves.
 typedef int v4i __attribute__((ext_vector_type(4)));
 
-__device__ inline uint32_t lds_addr(const void* p)
-{
-    return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
-}
-
+// 16-byte LDS read at a byte address (an ordinary load: the compiler places
+// the lgkmcnt wait before the first use of the value).
 template <int OFF> __device__ inline v4i lds_read16(uint32_t addr)
 {
-    v4i r;
-    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
-    return r;
+    return *(const __attribute__((address_space(3))) v4i*)(addr + OFF);
 }
 
-__device__ inline void lds_wait() { asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory"); }
-
-__device__ inline void lds_write8(uint32_t addr, uint2 v)
-{
-    asm volatile("ds_write_b64 %0, %1" : : "v"(addr), "v"(v) : "memory");
-}
-
-// After lds_wait(): tie a value read by lds_read16 to that point, so its uses
-// cannot move above the wait.
-__device__ inline void after_wait(v4i& a) { asm volatile("" : "+v"(a)); }
-
-// X slice layout in LDS: chunk (row r, 16-byte column chunk ch) at r * 4 + (ch ^ swz(r)).
+// X (and dense W) slice layout in LDS: chunk (row r, 16-byte column chunk ch)
+// at r * 4 + (ch ^ swz(r)).
 __device__ inline int xswz(int r) { return (r >> 1) & 3; }
-// Epilogue tile layout (64 rows of 64 bytes): chunk c of row r at c ^ eswz(r).
-__device__ inline int eswz(int r) { return (r >> 1) & 3; }
+
+// Walk entry (LDS table): {col | bits << 16 | last step of the item << 24 |
+// last entry of its segment << 25, first tile, start of the next segment in
+// this grid's item order, group}.  A slot's walk is cut into segments of at
+// most 64 entries; the producer holds one segment in VGPR lanes (lane i =
+// entry i) and the next one prefetched, so a step costs two lane reads and no
+// memory access.
+constexpr int W_LAST = 1 << 24, W_SEG_END = 1 << 25;
+constexpr int SEG = 64;
+// Queue entry of one step in flight (12 bits, up to 5 in a 64-bit queue): row
+// bits (8), last step of its item (bit 8), a real step (bit 9; entries past
+// the last item are 0).
+constexpr int E_LAST = 1 << 8, E_VALID = 1 << 9, E_BITS = 12, E_MASK = (1 << E_BITS) - 1;
 
 template <int DT, bool GELU, bool DENSE, bool KTAIL>
 __global__ __launch_bounds__(NT, 1) void k_linear16(
-    const Dims a, const char* __restrict__ X, const uint4* __restrict__ stream,
-    const int32_t* __restrict__ step_ptr, const int2* __restrict__ step_meta,
-    const int32_t* __restrict__ group_order, const char* __restrict__ W,
-    const uint32_t* __restrict__ bias32, char* __restrict__ Y)
+    const Dims a, const char* __restrict__ X, const char* __restrict__ stream,
+    const int4* __restrict__ gdesc, const int2* __restrict__ walk,
+    const char* __restrict__ W, const char* __restrict__ bias, char* __restrict__ Y)
 {
     using E = Elem<DT>;
     using F = typename E::frag;
-    __shared__ uint4 smem[NS * SLOT + NT / 64 * EPI_U4];
+    __shared__ uint4 smem[NS * SLOT + TAB_U4];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
     const int wm = wave & 3, wh = wave >> 2;
 
-    // this workgroup's items: k * P + item_off, k = 0, 1, ...
+    // this workgroup's items: k * P + item_off, k = 0, 1, ...; the 32 compute
+    // units of one XCD (blockIdx % 8) take 32 consecutive items
     const int P = (int)gridDim.x;
     const int item_off = (int)(blockIdx.x & 7) * (P >> 3) + (int)(blockIdx.x >> 3);
     const int my_items = item_off < a.n_items ? (a.n_items - item_off + P - 1) / P : 0;
     if (my_items == 0)
         return;
 
-    const char* zero = (const char*)g_zero;
-    const int last_col = a.n_tile_cols - 1;
-    const uint32_t smem0 = lds_addr(smem);
+    // ---- per-call tables in LDS: slot descriptors {group, first walk entry,
+    // walk length}, walk entries, float32 bias of each slot's 256 outputs
+    char* tab = (char*)(smem + NS * SLOT);
+    int4* t_desc = (int4*)tab;
+    int4* t_walk = (int4*)(tab + a.walk_off);
+    float* t_bias = (float*)(tab + a.bias_off);
+    const int ncol = a.n_tile_cols;
+    auto rows_of = [&](int g) { return (1 << min(G, a.n_tile_rows - g * G)) - 1; };
+    for (int i = tid; i < a.n_slots; i += NT) {
+        int4 d;
+        if (DENSE) {
+            d = make_int4(a.gs0 + i, i * ncol, ncol, 0);
+        } else {
+            d = gdesc[a.gs0 + i];
+            d.y -= a.walk0;
+        }
+        t_desc[i] = d;
+    }
+    __syncthreads();
+    for (int i = tid; i < a.n_walk; i += NT) {
+        int slot = 0;  // the slot whose walk holds entry i (few slots: linear search)
+        while (slot + 1 < a.n_slots && t_desc[slot + 1].y <= i)
+            ++slot;
+        const int4 d = t_desc[slot];
+        const int j = i - d.y;  // position in the slot's walk
+        int2 e;
+        if (DENSE) {
+            int col = (int)((int64_t)(a.gs0 + slot) * ncol / a.n_groups) + j;
+            if (col >= ncol)
+                col -= ncol;
+            e = make_int2(col | (rows_of(d.x) << 16) | (j == ncol - 1 ? W_LAST : 0), 0);
+        } else {
+            e = walk[a.walk0 + i];
+        }
+        const bool seg_end = (j % SEG == SEG - 1) || (j == d.z - 1);
+        int next = d.y + (j / SEG + 1) * SEG;  // the slot's next segment ...
+        if (j / SEG + 1 >= (d.z + SEG - 1) / SEG) {  // ... or the next item's first
+            int ns = slot + a.p_mod;
+            if (ns >= a.n_slots)
+                ns -= a.n_slots;
+            next = t_desc[ns].y;
+        }
+        t_walk[i] = make_int4(e.x | (seg_end ? W_SEG_END : 0), e.y, next, d.x);
+    }
+    for (int i = tid; i < a.n_slots * G * TILE; i += NT) {
+        const int64_t n = (int64_t)t_desc[i / (G * TILE)].x * G * TILE + i % (G * TILE);
+        t_bias[i] = (bias && n < a.N) ? E::to_f32(((const uint16_t*)bias)[n]) : 0.0f;
+    }
+    __syncthreads();
 
-    // Per-lane constants of this wave's DMA instructions.  X: LDS chunk p of
-    // the slice holds row p / 4, column chunk (p % 4) ^ swz(row).  W: chunk q
-    // of the step's operand-order tiles (dense: tile q / 128, lane q % 64 of
-    // k-step (q / 64) % 2).
-    int xrow[2], xcol[2], wrow[2], wcol[2];
+    const char* zero = (const char*)g_zero;
+    const uint32_t smem0 = lds_addr(smem);
+    const uint32_t walk_lds = lds_addr(t_walk), desc_lds = lds_addr(t_desc), bias_lds = lds_addr(t_bias);
+
+    // Per-lane constants of this wave's DMA instructions.  X / dense W: LDS
+    // chunk p of the slice holds row p / 4, column chunk (p % 4) ^ swz(row).
+    int srow[2], scol[2];
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
         const int p = (wave * 2 + i) * 64 + lane;
-        xrow[i] = p >> 2;
-        xcol[i] = ((p & 3) ^ xswz(p >> 2)) * 8;
-        wrow[i] = (p >> 7) * TILE + (p & 31);
-        wcol[i] = ((p >> 6) & 1) * 16 + ((p >> 5) & 1) * 8;
+        srow[i] = p >> 2;
+        scol[i] = ((p & 3) ^ xswz(p >> 2)) * 8;
     }
 
-    auto group_of = [&](int k, int& g, int& mt) {
-        const int it = k * P + item_off;
-        mt = it / a.n_groups;
-        const int gs = it - mt * a.n_groups;
-        g = DENSE ? gs : group_order[gs];
-    };
-    auto steps_of = [&](int g, int& s0, int& s1) {
-        if (DENSE) {
-            s0 = 0;
-            s1 = a.n_tile_cols;
-        } else {
-            s0 = step_ptr[g];
-            s1 = step_ptr[g + 1];
-        }
-    };
-
-    // ---- producer: the DMA cursor runs D steps ahead, across items.  Every
-    // wave issues exactly 2 X and 2 W DMA instructions per step: X rows past M
-    // repeat row M - 1 (their outputs are never stored); W chunks past the
-    // step's kept tiles fetch the tiles that follow (the stream is padded), and
-    // land in slot space nobody reads.
-    int pk = -1, ps = 0, ps_end = 0;
-    const char* xsrc[2];  // X[min(m0 + row, M - 1)][col chunk] at column tile 0
-    const char* wsrc[2];  // dense: W[min(g * 256 + row, N - 1)][col chunk]
-    auto next_item = [&]() {
-        while (++pk < my_items) {
-            int g, mt;
-            group_of(pk, g, mt);
-            steps_of(g, ps, ps_end);
-            if (ps < ps_end) {
+    // ---- producer: item pk (slot p_slot of token tile p_mt), segment
+    // entries in lanes (cur) and the next segment (nxt), position p_i
+    int pk = 0;
+    int p_mt = item_off / a.n_slots;
+    int p_slot = item_off - p_mt * a.n_slots;
+    // X of the producer's item: a uniform base (first row of the token tile)
+    // and per-lane byte offsets of row min(row, M - 1 - m0), column chunk
+    const char* xbase;
+    uint32_t xoff[2];
+    auto set_x = [&]() {
+        const int64_t m0 = (int64_t)p_mt * BM;
+        xbase = X + m0 * a.ldx * 2;
+        const int last_row = (int)min((int64_t)BM - 1, a.M - 1 - m0);
 #pragma unroll
-                for (int i = 0; i < 2; ++i) {
-                    const int64_t m = min((int64_t)mt * BM + xrow[i], a.M - 1);
-                    xsrc[i] = X + (m * a.ldx + xcol[i]) * 2;
-                    const int64_t n = min((int64_t)g * G * TILE + wrow[i], a.N - 1);
-                    wsrc[i] = DENSE ? W + (n * a.ldw + wcol[i]) * 2 : zero;
-                }
-                return;
-            }
-        }
+        for (int i = 0; i < 2; ++i)
+            xoff[i] = (uint32_t)((min(srow[i], last_row) * a.ldx + scol[i]) * 2);
     };
-    // The DMA of one step: sources and LDS destinations of this wave's 4
-    // instructions.  `meta` is step_meta[ps], loaded by the caller ahead of
-    // time (sparse only).
+    set_x();
+    // dense W: per-lane byte offsets within a group's first row
+    uint32_t woff[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+        woff[i] = (uint32_t)((srow[i] * a.ldw + scol[i]) * 2);
+    const uint32_t loff = (uint32_t)lane * 16;  // sparse W: lane's chunk of a tile
+    auto seg_read = [&](int start) {
+        return lds_read16<0>(walk_lds + min(start + lane, a.n_walk - 1) * 16);
+    };
+    int p_i = 0;
+    v4i cur = *(const v4i*)&t_walk[min(t_desc[p_slot].y + lane, a.n_walk - 1)];
+    v4i nxt = *(const v4i*)&t_walk[min(__builtin_amdgcn_readlane(cur.z, 0) + lane, a.n_walk - 1)];
+
+    // One step's DMA for this wave: uniform bases (X slice, W tiles or dense W
+    // rows), the ring slot, and the instruction count (2 or 4).
     struct Dma {
-        const char* src[4];
-        uint4* dst[4];
+        const char* xb;
+        const char* wb;
+        int slot, n, col;
+        int wlast;  // dense: last row of W inside the group (lanes past it repeat it)
     };
-    auto dma_prep = [&](int slot, int2 meta, Dma& d) {
-        uint4* xdst = smem + slot * SLOT + wave * 128;
-        uint4* wdst = smem + slot * SLOT + XU4 + wave * 128;
-        d.dst[0] = xdst;
-        d.dst[1] = xdst + 64;
-        d.dst[2] = wdst;
-        d.dst[3] = wdst + 64;
-        if (pk < my_items) {
-            const int col = DENSE ? ps : (meta.x & 0xffff);
-            const int64_t coff = (int64_t)col * TILE * 2;  // bytes to column tile col
-            d.src[0] = xsrc[0] + coff;
-            d.src[1] = xsrc[1] + coff;
-            if (DENSE) {
-                d.src[2] = wsrc[0] + coff;
-                d.src[3] = wsrc[1] + coff;
-            } else {
-                const char* tiles = (const char*)stream + (int64_t)meta.y * 2048 + wave * 2048;
-                d.src[2] = tiles + lane * 16;
-                d.src[3] = tiles + 1024 + lane * 16;
-            }
-            if (KTAIL && col == last_col) {  // columns past K read the zero line
-                if (col * TILE + xcol[0] >= a.K) d.src[0] = zero;
-                if (col * TILE + xcol[1] >= a.K) d.src[1] = zero;
-                if (DENSE && col * TILE + wcol[0] >= a.K) d.src[2] = zero;
-                if (DENSE && col * TILE + wcol[1] >= a.K) d.src[3] = zero;
-            }
+    auto p_prepare = [&](int slot, Dma& d) -> int {
+        d.slot = slot;
+        if (pk >= my_items) {
+            d.n = 0;
+            return 0;
+        }
+        const int ex = __builtin_amdgcn_readlane(cur.x, p_i);
+        const int col = ex & 0xffff, bits = (ex >> 16) & 0xff;
+        d.col = col;
+        d.xb = xbase + col * TILE * 2;
+        d.n = 2;
+        if (DENSE) {
+            const int64_t n0 = (int64_t)__builtin_amdgcn_readlane(cur.w, p_i) * G * TILE;
+            d.wb = W + n0 * a.ldw * 2 + col * TILE * 2;
+            d.wlast = (int)min((int64_t)G * TILE - 1, a.N - 1 - n0);
+            d.n = 4;
+        } else if ((bits >> wave) & 1) {  // row `wave` of the group is kept: its tile
+            const int rank = __popc(bits & ((1 << wave) - 1));
+            d.wb = stream + ((int64_t)__builtin_amdgcn_readlane(cur.y, p_i) + rank) * 2048;
+            d.n = 4;
+        }
+        const int e = bits | ((ex & W_LAST) ? E_LAST : 0) | E_VALID;
+        // advance: next entry of the segment, or the next segment (whose
+        // successor is read now; every half step waits for LDS reads)
+        if (ex & W_SEG_END) {
+            cur = nxt;
+            p_i = 0;
+            nxt = seg_read(__builtin_amdgcn_readlane(cur.z, 0));
         } else {
-            // past the last step: the same instruction count, into a free slot
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-                d.src[i] = zero;
+            ++p_i;
+        }
+        if ((ex & W_LAST) && ++pk < my_items) {
+            p_slot += a.p_mod;
+            p_mt += a.p_div;
+            if (p_slot >= a.n_slots) {
+                p_slot -= a.n_slots;
+                ++p_mt;
+            }
+            set_x();
+        }
+        return e;
+    };
+    // Instruction j (0, 1: X; 2, 3: W) of a prepared step.
+    auto dma_issue = [&](const Dma& d, int j) {
+        uint4* dst = smem + d.slot * SLOT + (j < 2 ? 0 : XU4) + wave * 128 + (j & 1) * 64;
+        const bool ktail = KTAIL && d.col == ncol - 1;  // columns past K read the zero line
+        if (j < 2) {
+            if (ktail && d.col * TILE + scol[j] >= a.K)
+                dma16(zero, dst);
+            else
+                dma16(d.xb, xoff[j], dst);
+        } else if (DENSE) {
+            const int i = j - 2;
+            uint32_t off = woff[i];
+            if (d.wlast < G * TILE - 1 && srow[i] > d.wlast)
+                off = (uint32_t)((d.wlast * a.ldw + scol[i]) * 2);
+            if (ktail && d.col * TILE + scol[i] >= a.K)
+                dma16(zero, dst);
+            else
+                dma16(d.wb, off, dst);
+        } else {
+            dma16(d.wb, loff + (j & 1) * 1024, dst);
         }
     };
-    auto dma_advance = [&]() {
-        if (pk < my_items && ++ps >= ps_end)
-            next_item();
-    };
-    auto produce = [&](int slot, int2 meta) {
-        Dma d;
-        dma_prep(slot, meta, d);
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-            dma16(d.src[i], d.dst[i]);
-        dma_advance();
+
+    // All instructions of a prepared step: its X, then its W if any.
+    auto dma_all = [&](const Dma& d) {
+        if (d.n >= 2) {
+            dma_issue(d, 0);
+            dma_issue(d, 1);
+            if (d.n == 4) {
+                dma_issue(d, 2);
+                dma_issue(d, 3);
+            }
+        }
     };
 
-    next_item();
-    int2 pmeta = make_int2(0, 0);  // step_meta at the producer cursor
+    // ---- prologue: the first D steps
+    uint64_t q = 0;  // queue entries of steps t, t + 1, ... (E_BITS each)
 #pragma unroll
     for (int i = 0; i < D; ++i) {
-        if (!DENSE)
-            pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
-        produce(i, pmeta);
+        Dma d;
+        q |= (uint64_t)(uint32_t)p_prepare(i, d) << (E_BITS * i);
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            if (j < d.n)
+                dma_issue(d, j);
     }
-    if (!DENSE)
-        pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
 
-    // LDS read addresses of this lane (slot 0; u = 1 is +2048 bytes, W ks = 1 is +1024)
-    uint32_t xa_addr[2];
+    // LDS read addresses of this lane (slot 0; token half u = 1 is +2048 bytes)
+    uint32_t xa_addr[2], wd_addr[2];
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
         const int r = wm * 64 + (lane & 31);
         const int ch = ks * 2 + (lane >> 5);
         xa_addr[ks] = smem0 + (r * 4 + (ch ^ xswz(r))) * 16;
+        const int rw = wh * 128 + (lane & 31);  // dense: tile row 4h + j is +j * 2048
+        wd_addr[ks] = smem0 + XU4 * 16 + (rw * 4 + (ch ^ xswz(rw))) * 16;
     }
-    const uint32_t wa_addr = smem0 + XU4 * 16 + lane * 16;
-    const uint32_t ebase = smem0 + NS * SLOT * 16 + wave * (EPI_U4 * 16);
+    const uint32_t wa_addr = smem0 + XU4 * 16 + wh * 4 * 2048 + lane * 16;  // this half's rows
 
-    // Step 0 has landed everywhere before anyone reads it.
-    wait_vm_lgkm0<LPS * (D - 1)>();
-    barrier_step();
+    // Operands of one half step (one 16-column k-step of a column tile): this
+    // wave's two X fragments (token halves) and its kept W fragments.
+    struct Ops {
+        v4i x[2], w[4];
+    };
+    // LDS reads of half step (t, ks)
+    auto read_half = [&](Ops& o, int t, int ks) {
+        const uint32_t slot_off = (uint32_t)(t & (NS - 1)) * (SLOT * 16);
+        o.x[0] = lds_read16<0>(xa_addr[ks] + slot_off);
+        o.x[1] = lds_read16<2048>(xa_addr[ks] + slot_off);
+        // four W fragments whatever the mask (no branch): rows 4h .. 4h + 3
+        // of the group, at fixed offsets in both layouts
+        if (DENSE) {
+            o.w[0] = lds_read16<0 * 2048>(wd_addr[ks] + slot_off);
+            o.w[1] = lds_read16<1 * 2048>(wd_addr[ks] + slot_off);
+            o.w[2] = lds_read16<2 * 2048>(wd_addr[ks] + slot_off);
+            o.w[3] = lds_read16<3 * 2048>(wd_addr[ks] + slot_off);
+        } else {
+            // row j of the group's tile lies at W position j (a dropped row's
+            // position holds stale data and is never used)
+            const uint32_t wa = wa_addr + slot_off + ks * 1024;
+            o.w[0] = lds_read16<0 * 2048>(wa);
+            o.w[1] = lds_read16<1 * 2048>(wa);
+            o.w[2] = lds_read16<2 * 2048>(wa);
+            o.w[3] = lds_read16<3 * 2048>(wa);
+        }
+    };
 
+    // consumer cursor
+    int ck = 0;
+    int c_mt = item_off / a.n_slots;
+    int c_slot = item_off - c_mt * a.n_slots;
+    int sp = 0;  // barriers still to pass while an item's stores may be in flight
+
+    // Accumulators start at the bias of their outputs: lane l, register 4 qq
+    // + i of tile row j holds output 8 qq + 4 (l / 32) + i of that row.
     f32x16 acc[2][4];
-    int t = 0;     // steps consumed
-    int e = -16;   // last step of the last item written out
-    for (int ck = 0; ck < my_items; ++ck) {
-        int g, mt, s0, s1;
-        group_of(ck, g, mt);
-        steps_of(g, s0, s1);
-        const int rows = (1 << min(G, a.n_tile_rows - g * G)) - 1;
-#pragma unroll
-        for (int u = 0; u < 2; ++u)
-#pragma unroll
-            for (int j = 0; j < 4; ++j)
-#pragma unroll
-                for (int v = 0; v < 16; ++v)
-                    acc[u][j][v] = 0.0f;
-
-        // One step.  The two waves of a SIMD take turns: group A (row half 0)
-        // reads its operands after the step's barrier and then runs the matrix
-        // cores; group B (row half 1) reads before the barrier and computes
-        // after it, so one wave's LDS reads overlap the other's MFMAs.  Before
-        // the barrier of step u every wave has waited for its DMA of step
-        // u + 1 (group B reads that step before the next barrier); after it,
-        // the slot of step u - 1 is free and is refilled with step u + D.  The
-        // wait also covers an epilogue's stores when one was issued after that
-        // DMA.  Metadata of the next step is loaded a step ahead.
-        int bits = DENSE ? rows : (s0 < s1 ? (step_meta[s0].x >> 16) : 0);
-        auto step = [&](int s) {
-            const int cur = bits;
-            if (!DENSE)
-                bits = s + 1 < s1 ? (step_meta[s + 1].x >> 16) : 0;
-            const uint32_t slot_off = (uint32_t)(t & (NS - 1)) * (SLOT * 16);
-            const int bh = (cur >> (4 * wh)) & 15;
-            v4i xa[2][2], wf[4][2];
-            auto read_ops = [&]() {
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks) {
-                    xa[0][ks] = lds_read16<0>(xa_addr[ks] + slot_off);
-                    xa[1][ks] = lds_read16<2048>(xa_addr[ks] + slot_off);
-                }
-                uint32_t wa = wa_addr + slot_off + (wh ? __popc(cur & 15) * 2048 : 0);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if (bh & (1 << j)) {
-                        wf[j][0] = lds_read16<0>(wa);
-                        wf[j][1] = lds_read16<1024>(wa);
-                        wa += 2048;
-                    }
-                }
-            };
-            auto sync = [&]() {
-                if (e >= t - 2)
-                    wait_vm_lgkm0<WAIT_B>();
-                else
-                    wait_vm_lgkm0<WAIT_A>();
-                barrier_step();
-            };
-            Dma dm;
-            if (wh == 0) {
-                sync();
-                read_ops();
-                dma_prep((t + D) & (NS - 1), pmeta, dm);
-                lds_wait();
-            } else {
-                read_ops();
-                lds_wait();
-                sync();
-                dma_prep((t + D) & (NS - 1), pmeta, dm);
-            }
-#pragma unroll
-            for (int u = 0; u < 2; ++u)
-#pragma unroll
-                for (int ks = 0; ks < 2; ++ks)
-                    after_wait(xa[u][ks]);
-            // the refill of the freed slot goes out one instruction at a time
-            // between the matrix-core instructions
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                dma16(dm.src[j], dm.dst[j]);
-                if (bh & (1 << j)) {
-                    after_wait(wf[j][0]);
-                    after_wait(wf[j][1]);
-                    const F w0 = __builtin_bit_cast(F, wf[j][0]);
-                    const F w1 = __builtin_bit_cast(F, wf[j][1]);
-                    acc[0][j] = E::mma(w0, __builtin_bit_cast(F, xa[0][0]), acc[0][j]);
-                    acc[1][j] = E::mma(w0, __builtin_bit_cast(F, xa[1][0]), acc[1][j]);
-                    acc[0][j] = E::mma(w1, __builtin_bit_cast(F, xa[0][1]), acc[0][j]);
-                    acc[1][j] = E::mma(w1, __builtin_bit_cast(F, xa[1][1]), acc[1][j]);
-                }
-            }
-            dma_advance();
-            if (!DENSE)
-                pmeta = pk < my_items ? step_meta[ps] : make_int2(0, 0);
-            ++t;
-        };
-        for (int s = s0; s < s1; ++s)
-            step(s);
-        e = t - 1;
-
-        // ---- epilogue: bias, GELU, one rounding; each wave transposes one
-        // 64 x 32 tile at a time through its own 4 KB of LDS, then stores 16
-        // bytes per lane, 64 contiguous bytes per row: exactly NSTORE store
-        // instructions per wave.  The stores are non-temporal: Y is not read
-        // again, and keeping it out of L2 leaves L2 to X and the tile stream.
-        const int h = lane >> 5;
+    const int h = lane >> 5;
+    auto init_acc = [&](int slot) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int64_t n_tile = (int64_t)(g * G + wh * 4 + j) * TILE;
-            uint32_t bw[16];
+            f32x16 b;
 #pragma unroll
-            for (int d = 0; d < 16; ++d)
-                bw[d] = 0u;
-            if (bias32) {
-                if (n_tile + TILE <= a.N) {
+            for (int qq = 0; qq < 4; ++qq) {
+                const v4i v = lds_read16<0>(bias_lds + (slot * G * TILE + (wh * 4 + j) * 32 + 8 * qq + 4 * h) * 4);
+                // (int) v[i], an rvalue: this compiler bit-casts a vector
+                // element lvalue as if it were element 0
 #pragma unroll
-                    for (int d = 0; d < 16; ++d)
-                        bw[d] = bias32[n_tile / 2 + d];
-                } else if (n_tile < a.N) {  // ragged last tile row (N % 32 == 16)
-#pragma unroll
-                    for (int d = 0; d < 8; ++d)
-                        bw[d] = bias32[n_tile / 2 + d];
-                }
+                for (int i = 0; i < 4; ++i)
+                    b[4 * qq + i] = __builtin_bit_cast(float, (int)v[i]);
             }
+            acc[0][j] = b;
+            acc[1][j] = b;
+        }
+    };
+
+    // Steps 0 .. D - 1 have landed everywhere before anyone reads step 0;
+    // the first half step's operands are read ahead of the loop.
+    __builtin_amdgcn_s_waitcnt(0);
+    barrier_step();
+    init_acc(c_slot);
+    Ops r0, r1;
+    read_half(r0, 0, 0);
+
+    // Barrier k means, for every wave: the DMA of step k + 1 has landed, and
+    // the slot of step k - 1 is free.
+    // first half of step t: the second half's operands are read and the refill
+    // DMA is issued, then (t, k-step 0) goes to the matrix cores
+    auto half_a = [&](int t, int bits, const Dma& dm) {
+        const int bh = (bits >> (4 * wh)) & 15;
+        read_half(r1, t, 1);
+        dma_all(dm);
 #pragma unroll
-            for (int u = 0; u < 2; ++u) {
-                const int r = u * 32 + (lane & 31);  // token row within the wave's 64
-#pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const uint32_t d0 = h ? bw[4 * q + 2] : bw[4 * q];
-                    const uint32_t d1 = h ? bw[4 * q + 3] : bw[4 * q + 1];
-                    float v[4] = {acc[u][j][4 * q] + E::to_f32(d0 & 0xffff),
-                                  acc[u][j][4 * q + 1] + E::to_f32(d0 >> 16),
-                                  acc[u][j][4 * q + 2] + E::to_f32(d1 & 0xffff),
-                                  acc[u][j][4 * q + 3] + E::to_f32(d1 >> 16)};
-                    if (GELU) {
-#pragma unroll
-                        for (int x = 0; x < 4; ++x)
-                            v[x] = gelu_erf(v[x]);
-                    }
-                    uint2 o;
-                    o.x = (uint32_t)E::from_f32(v[0]) | ((uint32_t)E::from_f32(v[1]) << 16);
-                    o.y = (uint32_t)E::from_f32(v[2]) | ((uint32_t)E::from_f32(v[3]) << 16);
-                    // row r, outputs 8q + 4h .. + 3: 16-byte chunk q ^ eswz(r), half h
-                    lds_write8(ebase + r * 64 + ((q ^ eswz(r)) * 16) + h * 8, o);
-                }
-            }
-            v4i ov[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const int r = i * 16 + (lane >> 2), c = lane & 3;
-                ov[i] = lds_read16<0>(ebase + r * 64 + ((c ^ eswz(r)) * 16));
-            }
-            lds_wait();
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                after_wait(ov[i]);
-                const int r = i * 16 + (lane >> 2), c = lane & 3;
-                const int64_t m = (int64_t)mt * BM + wm * 64 + r;
-                const int64_t n = n_tile + c * 8;
-                uint4* dst = (m < a.M && n < a.N) ? (uint4*)(Y + (m * a.ldy + n) * 2) : &g_sink[lane];
-                __builtin_nontemporal_store(ov[i], (v4i*)dst);
+        for (int j = 0; j < 4; ++j) {
+            if (bh & (1 << j)) {
+                const F wj = __builtin_bit_cast(F, r0.w[j]);
+                acc[0][j] = E::mma(wj, __builtin_bit_cast(F, r0.x[0]), acc[0][j]);
+                acc[1][j] = E::mma(wj, __builtin_bit_cast(F, r0.x[1]), acc[1][j]);
             }
         }
+    };
+    // second half of step t: (t, k-step 1) while the first half of step t + 1
+    // is read (its DMA landed before step t's barrier)
+    auto half_b = [&](int t, int bits) {
+        const int bh = (bits >> (4 * wh)) & 15;
+        read_half(r0, t + 1, 0);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (bh & (1 << j)) {
+                const F wj = __builtin_bit_cast(F, r1.w[j]);
+                acc[0][j] = E::mma(wj, __builtin_bit_cast(F, r1.x[0]), acc[0][j]);
+                acc[1][j] = E::mma(wj, __builtin_bit_cast(F, r1.x[1]), acc[1][j]);
+            }
+        }
+    };
+    // epilogue of item ck; false once this workgroup's items are done
+    auto epilogue = [&]() -> bool {
+        // ---- epilogue of item ck: GELU, one rounding.  Per 32 x 32 tile,
+            // lane l holds token l % 32 and outputs 8 q + 4 h + (0..3); swapping
+            // the q-even / q-odd halves between lanes l and l + 32 leaves each lane
+            // 8 consecutive outputs of its token, stored as 16 bytes: 2 stores per
+            // tile, NSTORE per wave and item, no LDS.
+            const v4i cd = lds_read16<0>(desc_lds + c_slot * 16);
+            const int c_g = __builtin_amdgcn_readfirstlane(cd.x);
+            const int64_t m0 = (int64_t)c_mt * BM + wm * 64 + (lane & 31);
+            const int64_t n0 = (int64_t)c_g * G * TILE + wh * 128 + 8 * h;
+            const bool inside = (int64_t)c_mt * BM + BM <= a.M && (int64_t)(c_g + 1) * G * TILE <= a.N;
+            char* ybase[2];
+#pragma unroll
+            for (int u = 0; u < 2; ++u)
+                ybase[u] = Y + ((m0 + 32 * u) * a.ldy + n0) * 2;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    uint32_t pk[4][2];
+#pragma unroll
+                    for (int qq = 0; qq < 4; ++qq) {
+                        float v[4] = {acc[u][j][4 * qq], acc[u][j][4 * qq + 1], acc[u][j][4 * qq + 2],
+                                      acc[u][j][4 * qq + 3]};
+                        if (GELU) {
+#pragma unroll
+                            for (int x = 0; x < 4; ++x)
+                                v[x] = gelu_erf(v[x]);
+                        }
+                        pk[qq][0] = pack2<DT>(v[0], v[1]);
+                        pk[qq][1] = pack2<DT>(v[2], v[3]);
+                    }
+#pragma unroll
+                    for (int p2 = 0; p2 < 2; ++p2) {
+                        // lanes < 32 keep q = 2 p2 and take it from lane + 32; lanes
+                        // >= 32 keep q = 2 p2 + 1 and take it from lane - 32
+                        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * p2][0], pk[2 * p2 + 1][0], false, false);
+                        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * p2][1], pk[2 * p2 + 1][1], false, false);
+                        v4i o;
+                        o.x = (int)s0[0];
+                        o.y = (int)s1[0];
+                        o.z = (int)s0[1];
+                        o.w = (int)s1[1];
+                        v4i* dst = (v4i*)(ybase[u] + (j * 32 + 16 * p2) * 2);
+                        if (!inside) {
+                            const int64_t m = m0 + 32 * u, n = n0 + j * 32 + 16 * p2;
+                            if (!(m < a.M && n < a.N))
+                                dst = (v4i*)&g_sink[lane];
+                        }
+                        *dst = o;
+                    }
+                }
+            }
+        if (++ck >= my_items)
+            return false;
+        c_slot += a.p_mod;
+        c_mt += a.p_div;
+        if (c_slot >= a.n_slots) {
+            c_slot -= a.n_slots;
+            ++c_mt;
+        }
+        init_acc(c_slot);
+        return true;
+    };
+
+    // wait until this wave's DMA of step k + 1 has landed (entry: the step
+    // after it, whose DMA may stay in flight), then barrier k.  Allowed in
+    // flight: the last 2 DMA instructions of that later step (its X; any W
+    // instructions come after them, so this may wait a little longer than
+    // needed) and, for the two barriers after an item's stores were issued
+    // behind this wave's DMA of step k + 1, those stores.
+    auto sync = [&](int entry) {
+        // case = (stores may be in flight) * 2 + (that later step is real)
+        const int cs = (sp > 0 ? 2 : 0) + ((entry >> 9) & 1);
+        sp = sp > 0 ? sp - 1 : 0;
+        if (DENSE)
+            step_barrier_wait<4>(cs);
+        else
+            step_barrier_wait<2>(cs);
+    };
+    for (int t = 0;; ++t) {
+        const int e0 = (int)(q & E_MASK);
+        Dma dx;
+        // barrier t; DMA of step t + 3 into the slot of step t - 1
+        sync((int)((q >> (2 * E_BITS)) & E_MASK));
+        q |= (uint64_t)(uint32_t)p_prepare((t + D) & (NS - 1), dx) << (3 * E_BITS);
+        half_a(t, e0 & 0xff, dx);
+        half_b(t, e0 & 0xff);
+        if (e0 & E_LAST) {
+            if (!epilogue())
+                break;
+            sp = 2;
+        }
+        q >>= E_BITS;
     }
-    // no DMA may still be writing this workgroup's LDS when it ends
+    // no DMA or store of this workgroup may be in flight when it ends
     __builtin_amdgcn_s_waitcnt(0);
 }
 
@@ -544,23 +662,60 @@ inline int num_cus()
     return n;
 }
 
+// Arguments of one k_linear16 launch.
+struct Args {
+    Dims d;
+    const char* X;
+    const char* stream;       // sparse: kept tiles in operand order
+    const int4* gdesc;        // sparse: launch slot descriptors
+    const int4* gdesc_host;   // sparse: their host copy (walk lengths)
+    const int2* walk;         // sparse: the slots' walks
+    const char* W;            // dense weight
+    const char* bias;
+    char* Y;
+};
+
 template <bool DENSE>
-hipError_t launch16(int dtype, bool gelu, const Args& a, hipStream_t s)
+hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
 {
-    if (a.d.n_items <= 0)
-        return hipSuccess;
-    int P = num_cus() & ~7;
-    const int need = (a.d.n_items + 7) / 8 * 8;
-    if (P < 8)
-        P = 8;
-    if (P > need)
-        P = need;
-    const dim3 grid(P), block(NT);
+    const int64_t n_mt = (a.d.M + BM - 1) / BM;
     const bool ktail = (a.d.K % TILE) != 0;
+    const int P0 = max(num_cus() & ~7, 8);
+    // Launches over consecutive launch slots whose tables fit the 16 KB of LDS
+    // reserved for them: 16 B per slot descriptor and walk entry, 1 KB of float32 bias
+    // per slot.
+    for (int gs0 = 0; gs0 < a.d.n_groups;) {
+        int ns = 0, nw = 0;
+        while (gs0 + ns < a.d.n_groups) {
+            const int len = DENSE ? a.d.n_tile_cols : a.gdesc_host[gs0 + ns].z;
+            if ((ns + 1) * (16 + G * TILE * 4) + (nw + len) * 16 > TAB_U4 * 16)
+                break;
+            ++ns;
+            nw += len;
+        }
+        if (ns == 0)
+            return hipErrorInvalidValue;  // one group's walk alone does not fit
+        Dims d = a.d;
+        d.gs0 = gs0;
+        d.n_slots = ns;
+        const int64_t items = n_mt * ns;
+        if (items > 0x7fffffff)
+            return hipErrorInvalidValue;
+        d.n_items = (int32_t)items;
+        d.walk0 = DENSE ? 0 : a.gdesc_host[gs0].y;
+        d.n_walk = nw;
+        d.walk_off = ns * 16;
+        d.bias_off = d.walk_off + nw * 16;
+        int P = P0;
+        const int need = (d.n_items + 7) / 8 * 8;
+        if (P > need)
+            P = need;
+        d.p_div = P / ns;
+        d.p_mod = P % ns;
+        const dim3 grid(P), block(NT);
 #define LPV_LAUNCH1(DT_, GELU_, KT_)                                                              \
-    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_>), grid, block, 0, s, a.d, a.X,         \
-                       a.stream, a.step_ptr, a.step_meta, a.group_order, a.W,                     \
-                       (const uint32_t*)a.bias, a.Y)
+    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_>), grid, block, 0, s, d, a.X, a.stream, \
+                       a.gdesc, a.walk, a.W, a.bias, a.Y)
 #define LPV_LAUNCH(DT_, GELU_)                                                                    \
     do {                                                                                          \
         if (ktail)                                                                                \
@@ -568,20 +723,25 @@ hipError_t launch16(int dtype, bool gelu, const Args& a, hipStream_t s)
         else                                                                                      \
             LPV_LAUNCH1(DT_, GELU_, false);                                                       \
     } while (0)
-    if (dtype == LPV_BF16) {
-        if (gelu)
-            LPV_LAUNCH(LPV_BF16, true);
-        else
-            LPV_LAUNCH(LPV_BF16, false);
-    } else {
-        if (gelu)
-            LPV_LAUNCH(LPV_F16, true);
-        else
-            LPV_LAUNCH(LPV_F16, false);
-    }
+        if (dtype == LPV_BF16) {
+            if (gelu)
+                LPV_LAUNCH(LPV_BF16, true);
+            else
+                LPV_LAUNCH(LPV_BF16, false);
+        } else {
+            if (gelu)
+                LPV_LAUNCH(LPV_F16, true);
+            else
+                LPV_LAUNCH(LPV_F16, false);
+        }
 #undef LPV_LAUNCH
 #undef LPV_LAUNCH1
-    return hipGetLastError();
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
+        gs0 += ns;
+    }
+    return hipSuccess;
 }
 
 Args base_args(const LinearCall& c, int64_t N, int64_t K)
@@ -595,7 +755,6 @@ Args base_args(const LinearCall& c, int64_t N, int64_t K)
     a.d.n_tile_rows = (int32_t)((N + TILE - 1) / TILE);
     a.d.n_tile_cols = (int32_t)((K + TILE - 1) / TILE);
     a.d.n_groups = (a.d.n_tile_rows + G - 1) / G;
-    a.d.n_items = (int32_t)((c.M + BM - 1) / BM) * a.d.n_groups;
     a.X = (const char*)c.X;
     a.bias = (const char*)c.bias;
     a.Y = (char*)c.Y;
@@ -629,10 +788,10 @@ hipError_t launch_bsr_linear(const lpv_bsr* h, const LinearCall& c, hipStream_t 
         return launch_f32<false>(c.gelu != 0, (const float*)c.X, c.ldx, c.M, h->K, h->N, h, nullptr,
                                  0, (const float*)c.bias, (float*)c.Y, c.ldy, s);
     Args a = base_args(c, h->N, h->K);
-    a.stream = (const uint4*)h->stream_vals;
-    a.step_ptr = h->step_ptr;
-    a.step_meta = h->step_meta;
-    a.group_order = h->group_order;
+    a.stream = (const char*)h->stream_vals;
+    a.gdesc = h->gdesc;
+    a.gdesc_host = h->gdesc_host;
+    a.walk = h->walk;
     return launch16<false>(h->dtype, c.gelu != 0, a, s);
 }
 

@@ -51,6 +51,20 @@ template <> struct Elem<1> {
 
 template <typename F> __device__ inline F as_frag(uint4 v) { return __builtin_bit_cast(F, v); }
 
+// Two float32 values rounded to nearest even and packed (low = a): one
+// v_cvt_pk_bf16_f32 / v_cvt_pk_f16_f32.
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+template <int DT> __device__ inline uint32_t pack2(float a, float b)
+{
+    const f32x2 v = {a, b};
+    if constexpr (DT == 2)
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2));
+    else
+        return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, f16x2));
+}
+
 // GELU with the exact error function (float32, device erff).
 __device__ inline float gelu_erf(float v) { return 0.5f * v * (1.0f + erff(v * 0.70710678118654752f)); }
 

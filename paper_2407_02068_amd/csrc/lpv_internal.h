@@ -18,7 +18,7 @@ constexpr int GROUP_TILES = 8;
 constexpr int BM = 256;
 
 struct Plan {  // sizes learnt on the device during pack
-    int32_t nnzb, n_steps, n_tiles, pad;
+    int32_t nnzb, n_steps, n_tiles, n_walk;
 };
 
 }  // namespace lpv
@@ -29,7 +29,7 @@ struct lpv_bsr {
     int64_t nnzb;
     int32_t dtype;  // lpv_dtype
     int32_t device;
-    void* meta;  // one allocation: row_ptr, group_order, step_ptr, group_tile0, plan
+    void* meta;  // one allocation: gdesc, row_ptr, group_order, step_ptr, group_tile0, plan
     // canonical BSR
     int32_t* row_ptr;  // R + 1
     int32_t* col_idx;  // nnzb
@@ -37,13 +37,16 @@ struct lpv_bsr {
     // tile schedule (16-bit element types only)
     int32_t n_tile_rows, n_tile_cols, n_groups;
     int64_t n_steps, n_tiles;
+    int4* gdesc;           // n_groups: {group, first walk entry, walk length, rotation} per launch slot
+    int4* gdesc_host;      // host copy of gdesc (sizes the linear kernel's launches)
     int32_t* group_order;  // n_groups
     int32_t* step_ptr;     // n_groups + 1
     int32_t* group_tile0;  // n_groups + 1, first stream tile of each group
     int32_t* step_col;     // n_steps
     int32_t* step_bits;    // n_steps
     int32_t* step_tile;    // n_steps
-    int2* step_meta;       // n_steps: {col | bits << 16, tile}, what the linear kernel reads
+    int64_t n_walk;
+    int2* walk;            // n_walk: the launch slots' walks, {col | bits << 16 | last << 24, tile}
     void* stream_vals;     // n_tiles * TILE * TILE elements, operand order
 };
 
@@ -60,7 +63,7 @@ struct PackArgs {
 
 // pack.hip
 hipError_t launch_pack_plan(const PackArgs& a, int32_t* row_ptr, int32_t* step_ptr,
-                            int32_t* group_tile0, int32_t* group_order, Plan* plan,
+                            int32_t* group_tile0, int32_t* group_order, int4* gdesc, Plan* plan,
                             hipStream_t s);
 hipError_t launch_pack_fill(const PackArgs& a, const lpv_bsr* h, hipStream_t s);
 hipError_t launch_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, hipStream_t s);

@@ -85,12 +85,15 @@ __device__ int block_exclusive_scan(int* arr, int n, int* s_wave, int* s_carry)
 __global__ __launch_bounds__(PLAN_THREADS) void k_pack_plan(PackArgs a, int32_t* row_ptr,
                                                             int32_t* step_ptr,
                                                             int32_t* group_tile0,
-                                                            int32_t* group_order, Plan* plan)
+                                                            int32_t* group_order, int4* gdesc,
+                                                            Plan* plan)
 {
     __shared__ int s_cnt[MAX_R];
     __shared__ int s_gsteps[MAX_GROUPS];
     __shared__ int s_gtiles[MAX_GROUPS];
     __shared__ int s_cost[MAX_GROUPS];
+    __shared__ int s_rank[MAX_GROUPS];
+    __shared__ int s_walk[MAX_GROUPS];
     __shared__ int s_wave[PLAN_WAVES];
     __shared__ int s_carry;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -139,6 +142,23 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_pack_plan(PackArgs a, int32_t*
             rank += (ch > cg) || (ch == cg && h < g);
         }
         group_order[rank] = g;
+        s_rank[g] = rank;
+        // steps walked for launch slot `rank`: an empty group still produces
+        // its bias, as one step with no tile
+        const int ns = (g + 1 < a.n_groups ? s_gsteps[g + 1] : n_steps) - s_gsteps[g];
+        s_walk[rank] = max(ns, 1);
+    }
+    __syncthreads();
+    // the launch slots' walks lie one after the other, in launch order
+    const int n_walk = block_exclusive_scan(s_walk, a.n_groups, s_wave, &s_carry);
+    for (int g = tid; g < a.n_groups; g += PLAN_THREADS) {
+        const int rank = s_rank[g];
+        const int ns = (g + 1 < a.n_groups ? s_gsteps[g + 1] : n_steps) - s_gsteps[g];
+        // the walk of slot `rank` starts at column step rank * ns / n_groups and
+        // wraps: slots that run side by side on one token tile read different X
+        // columns at a time
+        gdesc[rank] = make_int4(g, s_walk[rank], max(ns, 1),
+                                ns > 0 ? (int)((int64_t)rank * ns / a.n_groups) : 0);
     }
     if (tid == 0) {
         row_ptr[a.R] = nnzb;
@@ -147,7 +167,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_pack_plan(PackArgs a, int32_t*
         plan->nnzb = nnzb;
         plan->n_steps = n_steps;
         plan->n_tiles = n_tiles;
-        plan->pad = 0;
+        plan->n_walk = n_walk;
     }
 }
 
@@ -203,8 +223,7 @@ __global__ __launch_bounds__(64) void k_sched_fill(PackArgs a, const int32_t* __
                                                    const int32_t* __restrict__ group_tile0,
                                                    int32_t* __restrict__ step_col,
                                                    int32_t* __restrict__ step_bits,
-                                                   int32_t* __restrict__ step_tile,
-                                                   int2* __restrict__ step_meta)
+                                                   int32_t* __restrict__ step_tile)
 {
     const int g = blockIdx.x;
     int s = step_ptr[g], t = group_tile0[g];
@@ -219,7 +238,6 @@ __global__ __launch_bounds__(64) void k_sched_fill(PackArgs a, const int32_t* __
             step_col[pos] = tc;
             step_bits[pos] = bits;
             step_tile[pos] = t + inc - pc;
-            step_meta[pos] = make_int2(tc | (bits << 16), t + inc - pc);
         }
         s += __popcll(b);
         t += __shfl(inc, 63, 64);
@@ -267,6 +285,32 @@ __global__ __launch_bounds__(256) void k_stream_fill(PackArgs a, const int32_t* 
     }
 }
 
+// One wave per launch slot: the slot's walk, the group's steps starting at its
+// rotation and wrapping, as {col | bits << 16 | last << 24, first tile}.  An
+// empty group walks one step with no tile.
+__global__ __launch_bounds__(64) void k_walk_fill(const int4* __restrict__ gdesc,
+                                                  const int32_t* __restrict__ step_ptr,
+                                                  const int32_t* __restrict__ step_col,
+                                                  const int32_t* __restrict__ step_bits,
+                                                  const int32_t* __restrict__ step_tile,
+                                                  int2* __restrict__ walk)
+{
+    const int4 d = gdesc[blockIdx.x];  // group, first walk entry, walk length, rotation
+    const int s0 = step_ptr[d.x], ns = step_ptr[d.x + 1] - s0;
+    for (int i = threadIdx.x; i < d.z; i += 64) {
+        const int last = (i == d.z - 1) ? 1 << 24 : 0;
+        int2 e = make_int2(last, 0);
+        if (ns > 0) {
+            int j = d.w + i;
+            if (j >= ns)
+                j -= ns;
+            const int s = s0 + j;
+            e = make_int2(step_col[s] | (step_bits[s] << 16) | last, step_tile[s]);
+        }
+        walk[d.y + i] = e;
+    }
+}
+
 // One workgroup per block-row: the pruned dense rows, +0.0 in dropped blocks.
 __global__ __launch_bounds__(256) void k_unpack(int64_t K, int32_t b_r, int32_t b_c, int32_t C,
                                                 int32_t es, const int32_t* __restrict__ row_ptr,
@@ -300,12 +344,13 @@ __global__ __launch_bounds__(256) void k_unpack(int64_t K, int32_t b_r, int32_t 
 }  // namespace
 
 hipError_t launch_pack_plan(const PackArgs& a, int32_t* row_ptr, int32_t* step_ptr,
-                            int32_t* group_tile0, int32_t* group_order, Plan* plan, hipStream_t s)
+                            int32_t* group_tile0, int32_t* group_order, int4* gdesc, Plan* plan,
+                            hipStream_t s)
 {
     if (a.R > MAX_R || a.C > MAX_C || a.n_groups > MAX_GROUPS)
         return hipErrorInvalidValue;
     hipLaunchKernelGGL(k_pack_plan, dim3(1), dim3(PLAN_THREADS), 0, s, a, row_ptr, step_ptr,
-                       group_tile0, group_order, plan);
+                       group_tile0, group_order, gdesc, plan);
     return hipGetLastError();
 }
 
@@ -317,16 +362,20 @@ hipError_t launch_pack_fill(const PackArgs& a, const lpv_bsr* h, hipStream_t s)
         hipLaunchKernelGGL(k_pack_compact, dim3(a.R), dim3(256), 0, s, a, h->row_ptr, h->col_idx,
                            (char*)h->values);
     hipError_t e = hipGetLastError();
-    if (e != hipSuccess || h->stream_vals == nullptr)
+    // fp32 handles carry no schedule; a matrix-core handle always has a walk
+    // (one entry per empty group), even when no tile is kept
+    if (e != hipSuccess || h->walk == nullptr)
         return e;
     if (a.n_groups > 0)
         hipLaunchKernelGGL(k_sched_fill, dim3(a.n_groups), dim3(64), 0, s, a, h->step_ptr,
-                           h->group_tile0, h->step_col, h->step_bits, h->step_tile,
-                           h->step_meta);
+                           h->group_tile0, h->step_col, h->step_bits, h->step_tile);
     if (h->n_steps > 0)
         hipLaunchKernelGGL(k_stream_fill, dim3((unsigned)h->n_steps), dim3(256), 0, s, a,
                            h->step_ptr, h->step_col, h->step_bits, h->step_tile,
                            (uint4*)h->stream_vals);
+    if (a.n_groups > 0)
+        hipLaunchKernelGGL(k_walk_fill, dim3(a.n_groups), dim3(64), 0, s, h->gdesc, h->step_ptr,
+                           h->step_col, h->step_bits, h->step_tile, h->walk);
     return hipGetLastError();
 }
 

@@ -96,6 +96,8 @@ def dense(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, X=FAKE + (1 << 32), ldx=768, 
     (dict(X=0), INVALID), (dict(Y=0), INVALID), (dict(X=FAKE + (1 << 32) + 4), INVALID),
     (dict(bias=FAKE + 2), INVALID), (dict(epi=2), INVALID), (dict(W=0), INVALID),
     (dict(Y=FAKE + (1 << 32) + 64), ALIAS), (dict(X=FAKE + (2 << 32) + 1024), ALIAS),
+    # leading dimensions above 2^22 elements (32-bit byte offsets in the kernels)
+    (dict(ldx=(1 << 22) + 8), INVALID), (dict(ldw=(1 << 22) + 8), INVALID),
 ])
 def test_dense_rejects_bad_arguments(L, kw, want):
     assert dense(L, **kw) == want
