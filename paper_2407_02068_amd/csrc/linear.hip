@@ -161,12 +161,20 @@ typedef int v4i __attribute__((ext_vector_type(4)));
 // the lgkmcnt wait before the first use of the value).
 template <int OFF> __device__ inline v4i lds_read16(uint32_t addr)
 {
-    return *(const __attribute__((address_space(3))) v4i*)(addr + OFF);
+    return *(const __attribute__((address_space(3))) v4i*)(uintptr_t)(addr + OFF);
+}
+
+__device__ inline void lds_write16(uint32_t addr, v4i v)
+{
+    *(__attribute__((address_space(3))) v4i*)(uintptr_t)addr = v;
 }
 
 // X (and dense W) slice layout in LDS: chunk (row r, 16-byte column chunk ch)
-// at r * 4 + (ch ^ swz(r)).
-__device__ inline int xswz(int r) { return (r >> 1) & 3; }
+// at r * 4 + (ch ^ swz(r)).  A 16-byte read by 16 lanes (rows r .. r + 15 of
+// one chunk column) then touches 16 different 16-byte bank groups: the LDS
+// serves 256 bytes per clock, and rows 4 apart share a bank group unless the
+// swizzle separates them.
+__device__ inline int xswz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
 
 // Walk entry (LDS table): {col | bits << 16 | last step of the item << 24 |
 // last entry of its segment << 25, first tile, start of the next segment in
@@ -502,26 +510,37 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             }
         }
     };
-    // epilogue of item ck; false once this workgroup's items are done
-    auto epilogue = [&]() -> bool {
-        // ---- epilogue of item ck: GELU, one rounding.  Per 32 x 32 tile,
-            // lane l holds token l % 32 and outputs 8 q + 4 h + (0..3); swapping
-            // the q-even / q-odd halves between lanes l and l + 32 leaves each lane
-            // 8 consecutive outputs of its token, stored as 16 bytes: 2 stores per
-            // tile, NSTORE per wave and item, no LDS.
-            const v4i cd = lds_read16<0>(desc_lds + c_slot * 16);
-            const int c_g = __builtin_amdgcn_readfirstlane(cd.x);
-            const int64_t m0 = (int64_t)c_mt * BM + wm * 64 + (lane & 31);
-            const int64_t n0 = (int64_t)c_g * G * TILE + wh * 128 + 8 * h;
-            const bool inside = (int64_t)c_mt * BM + BM <= a.M && (int64_t)(c_g + 1) * G * TILE <= a.N;
-            char* ybase[2];
+    // ---- epilogue of item ck (GELU, one rounding), run after the barrier that
+    // frees the slot of the item's last step.  Per 32 x 32 tile, lane l holds
+    // token l % 32 and outputs 8 q + 4 h + (0..3); swapping the q-even / q-odd
+    // halves between lanes l and l + 32 leaves each lane 8 consecutive outputs
+    // (16 bytes) of its token.  These pass through this wave's own 4 KB of the
+    // freed slot (the parts its next DMA refills) so that every store writes
+    // 8 whole 128-byte lines of Y: lanes 8 i .. 8 i + 7 hold one token's 64
+    // consecutive outputs.  Streaming (non-temporal) stores keep the output
+    // from evicting X and W from the caches.  NSTORE stores per wave and item.
+    auto epilogue = [&](int sslot) {
+        const v4i cd = lds_read16<0>(desc_lds + c_slot * 16);
+        const int c_g = __builtin_amdgcn_readfirstlane(cd.x);
+        const int64_t mw = (int64_t)c_mt * BM + wm * 64;        // wave's first token
+        const int64_t nw = (int64_t)c_g * G * TILE + wh * 128;   // wave's first output
+        const bool inside = (int64_t)c_mt * BM + BM <= a.M && (int64_t)(c_g + 1) * G * TILE <= a.N;
+        // staging: token tau (0..31) of a round at region tau / 16 (X part,
+        // then W part of this wave's DMA area), row tau % 16 of 128 bytes,
+        // 16-byte chunk k at k ^ ((tau / 2) % 8): conflict-free both ways
+        const uint32_t st0 = smem0 + (uint32_t)(sslot * SLOT + wave * 128) * 16;
+        const uint32_t st1 = st0 + XU4 * 16;
+        const int b = lane & 31;
+        const uint32_t wbase = (b < 16 ? st0 : st1) + (b & 15) * 128;
+        const int wswz = (b >> 1) & 7;
 #pragma unroll
-            for (int u = 0; u < 2; ++u)
-                ybase[u] = Y + ((m0 + 32 * u) * a.ldy + n0) * 2;
+        for (int u = 0; u < 2; ++u) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j) {
+            for (int lam = 0; lam < 2; ++lam) {
+                // round (u, lam): tokens 32 u + 0..31, outputs 64 lam + 0..63
 #pragma unroll
-                for (int u = 0; u < 2; ++u) {
+                for (int jj = 0; jj < 2; ++jj) {
+                    const int j = 2 * lam + jj;
                     uint32_t pk[4][2];
 #pragma unroll
                     for (int qq = 0; qq < 4; ++qq) {
@@ -546,34 +565,31 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                         o.y = (int)s1[0];
                         o.z = (int)s0[1];
                         o.w = (int)s1[1];
-                        v4i* dst = (v4i*)(ybase[u] + (j * 32 + 16 * p2) * 2);
-                        if (!inside) {
-                            const int64_t m = m0 + 32 * u, n = n0 + j * 32 + 16 * p2;
-                            if (!(m < a.M && n < a.N))
-                                dst = (v4i*)&g_sink[lane];
-                        }
-                        *dst = o;
+                        const int k = jj * 4 + 2 * p2 + h;  // chunk of the 128-byte line
+                        lds_write16(wbase + ((k ^ wswz) * 16), o);
                     }
                 }
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int tau = 8 * i + (lane >> 3), k = lane & 7;
+                    const v4i o = lds_read16<0>((i < 2 ? st0 : st1) + (tau & 15) * 128 +
+                                                ((k ^ ((tau >> 1) & 7)) * 16));
+                    const int64_t m = mw + 32 * u + tau, n = nw + 64 * lam + 8 * k;
+                    v4i* dst = (v4i*)(Y + (m * a.ldy + n) * 2);
+                    if (!inside && !(m < a.M && n < a.N))
+                        dst = (v4i*)&g_sink[lane];
+                    __builtin_nontemporal_store(o, dst);
+                }
             }
-        if (++ck >= my_items)
-            return false;
-        c_slot += a.p_mod;
-        c_mt += a.p_div;
-        if (c_slot >= a.n_slots) {
-            c_slot -= a.n_slots;
-            ++c_mt;
         }
-        init_acc(c_slot);
-        return true;
     };
 
     // wait until this wave's DMA of step k + 1 has landed (entry: the step
     // after it, whose DMA may stay in flight), then barrier k.  Allowed in
     // flight: the last 2 DMA instructions of that later step (its X; any W
     // instructions come after them, so this may wait a little longer than
-    // needed) and, for the two barriers after an item's stores were issued
-    // behind this wave's DMA of step k + 1, those stores.
+    // needed) and, for the barrier after an item's stores were issued behind
+    // this wave's DMA of step k + 1, those stores.
     auto sync = [&](int entry) {
         // case = (stores may be in flight) * 2 + (that later step is real)
         const int cs = (sp > 0 ? 2 : 0) + ((entry >> 9) & 1);
@@ -583,19 +599,32 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         else
             step_barrier_wait<2>(cs);
     };
+    bool item_done = false;  // the previous step was its item's last
     for (int t = 0;; ++t) {
         const int e0 = (int)(q & E_MASK);
         Dma dx;
         // barrier t; DMA of step t + 3 into the slot of step t - 1
         sync((int)((q >> (2 * E_BITS)) & E_MASK));
+        if (item_done) {
+            // the stores go out before this step's DMA: the next barrier lets
+            // them stay in flight, the one after waits for them
+            epilogue((t - 1) & (NS - 1));
+            if (++ck >= my_items)
+                break;
+            sp = 1;
+            c_slot += a.p_mod;
+            c_mt += a.p_div;
+            if (c_slot >= a.n_slots) {
+                c_slot -= a.n_slots;
+                ++c_mt;
+            }
+            init_acc(c_slot);
+            item_done = false;
+        }
         q |= (uint64_t)(uint32_t)p_prepare((t + D) & (NS - 1), dx) << (3 * E_BITS);
         half_a(t, e0 & 0xff, dx);
         half_b(t, e0 & 0xff);
-        if (e0 & E_LAST) {
-            if (!epilogue())
-                break;
-            sp = 2;
-        }
+        item_done = (e0 & E_LAST) != 0;
         q >>= E_BITS;
     }
     // no DMA or store of this workgroup may be in flight when it ends
