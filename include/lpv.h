@@ -102,6 +102,8 @@ typedef struct {
  *
  * Allocates device memory (freed by lpv_bsr_destroy) and waits once on
  * `stream` to learn the kept count.  W and mask may be freed afterwards.
+ * bf16 / fp16: at most 2^21 - 1 kept 32 x 32 tiles (SHAPE otherwise; the
+ * kernels address the tile copy with 32-bit byte offsets).
  * Errors: INVALID_ARG, SHAPE, DTYPE, BLOCK, ALLOC, HIP.
  */
 lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,

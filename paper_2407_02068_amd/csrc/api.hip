@@ -240,6 +240,12 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
     h->n_steps = mfma_path ? plan.n_steps : 0;
     h->n_tiles = mfma_path ? plan.n_tiles : 0;
     h->n_walk = mfma_path ? plan.n_walk : 0;
+    if (h->n_tiles >= ((int64_t)1 << 21)) {
+        // the kernels address the tile stream with 32-bit byte offsets
+        const long long nt = (long long)h->n_tiles;
+        free_handle(h);
+        return fail(LPV_ERR_SHAPE, "%lld kept 32 x 32 tiles: at most 2^21 - 1 are supported", nt);
+    }
 
     const size_t blk = (size_t)b_r * b_c * es;
     e = dmalloc((void**)&h->col_idx, (size_t)h->nnzb * sizeof(int32_t));

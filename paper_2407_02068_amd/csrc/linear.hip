@@ -111,6 +111,19 @@ __device__ inline void dma16(const char* base, uint32_t off, uint4* lds_wave_bas
         : "memory");
 }
 
+// The same with the instruction offset IMM, which the hardware adds to both
+// the global and the LDS address (global: saddr + voff + IMM; LDS: M0 + IMM +
+// 16 * lane).  Two DMAs 1 KB apart in LDS share one M0 value this way.
+template <int IMM> __device__ inline void dma16i(const char* saddr, uint32_t voff, uint32_t m0)
+{
+    asm volatile(
+        "s_nop 0\n"
+        "global_load_lds_dwordx4 %0, %1 offset:%3"
+        :
+        : "v"(voff), "s"(saddr), "{m0}"(m0), "i"(IMM)
+        : "memory");
+}
+
 // s_waitcnt vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt left alone)
 template <int N> __device__ inline void wait_vm()
 {
@@ -119,32 +132,43 @@ template <int N> __device__ inline void wait_vm()
 }
 
 // The wait before a step barrier and the barrier, as one small branch tree
-// (the compiler spends several times the instructions on it): case 0: nothing
-// of this wave's may stay in flight; 1: its last N DMA instructions may; 2:
-// its last NSTORE stores may; 3: both.
-template <int N> __device__ inline void step_barrier_wait(int cs)
+// (the compiler spends several times the instructions on it).  Case 3 s + k:
+// this wave's last NSTORE * s + 2 k vector-memory instructions may stay in
+// flight (s: an item's stores, k: 0..2 pairs of DMA instructions).
+__device__ inline void step_barrier_wait(int cs)
 {
+    static_assert(NSTORE == 16, "vmcnt immediates below");
     asm volatile(
-        "s_cmp_lt_u32 %0, 2\n"
+        "s_cmp_lt_u32 %0, 3\n"
         "s_cbranch_scc1 1f\n"
         "s_cmp_eq_u32 %0, 3\n"
-        "s_cbranch_scc0 2f\n"
-        "s_waitcnt vmcnt(%1)\n"
-        "s_branch 4f\n"
-        "2:\n"
-        "s_waitcnt vmcnt(%2)\n"
-        "s_branch 4f\n"
-        "1:\n"
-        "s_cmp_eq_u32 %0, 1\n"
-        "s_cbranch_scc0 3f\n"
-        "s_waitcnt vmcnt(%3)\n"
-        "s_branch 4f\n"
-        "3:\n"
-        "s_waitcnt vmcnt(0)\n"
+        "s_cbranch_scc1 3f\n"
+        "s_cmp_eq_u32 %0, 4\n"
+        "s_cbranch_scc1 4f\n"
+        "s_waitcnt vmcnt(20)\n"
+        "s_branch 7f\n"
         "4:\n"
+        "s_waitcnt vmcnt(18)\n"
+        "s_branch 7f\n"
+        "3:\n"
+        "s_waitcnt vmcnt(16)\n"
+        "s_branch 7f\n"
+        "1:\n"
+        "s_cmp_eq_u32 %0, 0\n"
+        "s_cbranch_scc1 5f\n"
+        "s_cmp_eq_u32 %0, 1\n"
+        "s_cbranch_scc1 6f\n"
+        "s_waitcnt vmcnt(4)\n"
+        "s_branch 7f\n"
+        "6:\n"
+        "s_waitcnt vmcnt(2)\n"
+        "s_branch 7f\n"
+        "5:\n"
+        "s_waitcnt vmcnt(0)\n"
+        "7:\n"
         "s_barrier"
         :
-        : "s"(cs), "i"(N + NSTORE), "i"(NSTORE), "i"(N)
+        : "s"(cs)
         : "memory", "scc");
 }
 
@@ -280,24 +304,35 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     int pk = 0;
     int p_mt = item_off / a.n_slots;
     int p_slot = item_off - p_mt * a.n_slots;
-    // X of the producer's item: a uniform base (first row of the token tile)
-    // and per-lane byte offsets of row min(row, M - 1 - m0), column chunk
+    // X of the producer's item: a uniform base (first row of the token tile;
+    // the second instruction's base is 1 KB lower, see dma16i) and per-lane
+    // byte offsets of row min(row, M - 1 - m0), column chunk.  Dense W: the
+    // same for the item's group of output rows (rows past N repeat its last).
     const char* xbase;
+    const char* xbase_k;
     uint32_t xoff[2];
+    const char* wibase = nullptr;
+    const char* wibase_k = nullptr;
+    uint32_t wioff[2] = {0, 0};
     auto set_x = [&]() {
         const int64_t m0 = (int64_t)p_mt * BM;
         xbase = X + m0 * a.ldx * 2;
+        xbase_k = xbase - 1024;
         const int last_row = (int)min((int64_t)BM - 1, a.M - 1 - m0);
 #pragma unroll
         for (int i = 0; i < 2; ++i)
             xoff[i] = (uint32_t)((min(srow[i], last_row) * a.ldx + scol[i]) * 2);
+        if (DENSE) {
+            const int64_t n0 = (int64_t)t_desc[p_slot].x * G * TILE;
+            wibase = W + n0 * a.ldw * 2;
+            wibase_k = wibase - 1024;
+            const int wlast = (int)min((int64_t)G * TILE - 1, a.N - 1 - n0);
+#pragma unroll
+            for (int i = 0; i < 2; ++i)
+                wioff[i] = (uint32_t)((min(srow[i], wlast) * a.ldw + scol[i]) * 2);
+        }
     };
     set_x();
-    // dense W: per-lane byte offsets within a group's first row
-    uint32_t woff[2];
-#pragma unroll
-    for (int i = 0; i < 2; ++i)
-        woff[i] = (uint32_t)((srow[i] * a.ldw + scol[i]) * 2);
     const uint32_t loff = (uint32_t)lane * 16;  // sparse W: lane's chunk of a tile
     auto seg_read = [&](int start) {
         return lds_read16<0>(walk_lds + min(start + lane, a.n_walk - 1) * 16);
@@ -306,33 +341,39 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     v4i cur = *(const v4i*)&t_walk[min(t_desc[p_slot].y + lane, a.n_walk - 1)];
     v4i nxt = *(const v4i*)&t_walk[min(__builtin_amdgcn_readlane(cur.z, 0) + lane, a.n_walk - 1)];
 
-    // One step's DMA for this wave: uniform bases (X slice, W tiles or dense W
-    // rows), the ring slot, and the instruction count (2 or 4).
+    // One step's DMA for this wave: the ring slot, the instruction count (2 or
+    // 4), the column tile and its byte offset in a row of X / dense W, and
+    // (sparse) the byte offset of this wave's W tile in the tile stream.
     struct Dma {
-        const char* xb;
-        const char* wb;
         int slot, n, col;
-        int wlast;  // dense: last row of W inside the group (lanes past it repeat it)
+        uint32_t xcol, woff;
     };
+    bool x_stale = false;  // the item advanced: set_x() before the next step
     auto p_prepare = [&](int slot, Dma& d) -> int {
-        d.slot = slot;
-        if (pk >= my_items) {
-            d.n = 0;
-            return 0;
+        // (the previous step's DMA, issued after its p_prepare, used the old
+        // item's bases)
+        if (x_stale) {
+            set_x();
+            x_stale = false;
         }
+        d.slot = slot;
+        d.n = 0;
+        d.col = 0;
+        d.xcol = 0;
+        d.woff = 0;
+        if (pk >= my_items)
+            return 0;
         const int ex = __builtin_amdgcn_readlane(cur.x, p_i);
         const int col = ex & 0xffff, bits = (ex >> 16) & 0xff;
         d.col = col;
-        d.xb = xbase + col * TILE * 2;
+        d.xcol = (uint32_t)col * (TILE * 2);
         d.n = 2;
         if (DENSE) {
-            const int64_t n0 = (int64_t)__builtin_amdgcn_readlane(cur.w, p_i) * G * TILE;
-            d.wb = W + n0 * a.ldw * 2 + col * TILE * 2;
-            d.wlast = (int)min((int64_t)G * TILE - 1, a.N - 1 - n0);
             d.n = 4;
         } else if ((bits >> wave) & 1) {  // row `wave` of the group is kept: its tile
+            // (the stream holds fewer than 2^21 tiles: the offset fits 32 bits)
             const int rank = __popc(bits & ((1 << wave) - 1));
-            d.wb = stream + ((int64_t)__builtin_amdgcn_readlane(cur.y, p_i) + rank) * 2048;
+            d.woff = (uint32_t)(__builtin_amdgcn_readlane(cur.y, p_i) + rank) * 2048u;
             d.n = 4;
         }
         const int e = bits | ((ex & W_LAST) ? E_LAST : 0) | E_VALID;
@@ -352,41 +393,51 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                 p_slot -= a.n_slots;
                 ++p_mt;
             }
-            set_x();
+            x_stale = true;
         }
         return e;
     };
-    // Instruction j (0, 1: X; 2, 3: W) of a prepared step.
-    auto dma_issue = [&](const Dma& d, int j) {
+    // Instruction j (0, 1: X; 2, 3: W) of a prepared step, in the general form
+    // (last column tile of a K that is not a multiple of 32: lanes past K read
+    // the zero line).
+    auto dma_issue_tail = [&](const Dma d, int j) {
         uint4* dst = smem + d.slot * SLOT + (j < 2 ? 0 : XU4) + wave * 128 + (j & 1) * 64;
-        const bool ktail = KTAIL && d.col == ncol - 1;  // columns past K read the zero line
-        if (j < 2) {
-            if (ktail && d.col * TILE + scol[j] >= a.K)
+        const int i = j & 1;
+        if (j < 2 || DENSE) {
+            if (d.col * TILE + scol[i] >= a.K)
                 dma16(zero, dst);
+            else if (j < 2)
+                dma16(xbase, xoff[i] + d.xcol, dst);
             else
-                dma16(d.xb, xoff[j], dst);
-        } else if (DENSE) {
-            const int i = j - 2;
-            uint32_t off = woff[i];
-            if (d.wlast < G * TILE - 1 && srow[i] > d.wlast)
-                off = (uint32_t)((d.wlast * a.ldw + scol[i]) * 2);
-            if (ktail && d.col * TILE + scol[i] >= a.K)
-                dma16(zero, dst);
-            else
-                dma16(d.wb, off, dst);
+                dma16(wibase, wioff[i] + d.xcol, dst);
         } else {
-            dma16(d.wb, loff + (j & 1) * 1024, dst);
+            dma16(stream, loff + d.woff + i * 1024, dst);
         }
     };
 
-    // All instructions of a prepared step: its X, then its W if any.
-    auto dma_all = [&](const Dma& d) {
-        if (d.n >= 2) {
-            dma_issue(d, 0);
-            dma_issue(d, 1);
-            if (d.n == 4) {
-                dma_issue(d, 2);
-                dma_issue(d, 3);
+    // All instructions of a prepared step: its X, then its W if any.  X and W
+    // each take one M0 value for their two instructions.
+    auto dma_all = [&](const Dma d) {
+        if (d.n < 2)
+            return;
+        if (KTAIL && d.col == ncol - 1) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (j < d.n)
+                    dma_issue_tail(d, j);
+            return;
+        }
+        const uint32_t mx = smem0 + (uint32_t)(d.slot * SLOT + wave * 128) * 16;
+        dma16i<0>(xbase, xoff[0] + d.xcol, mx);
+        dma16i<1024>(xbase_k, xoff[1] + d.xcol, mx);
+        if (d.n == 4) {
+            const uint32_t mw = mx + XU4 * 16;
+            if (DENSE) {
+                dma16i<0>(wibase, wioff[0] + d.xcol, mw);
+                dma16i<1024>(wibase_k, wioff[1] + d.xcol, mw);
+            } else {
+                dma16i<0>(stream, loff + d.woff, mw);
+                dma16i<1024>(stream, loff + d.woff, mw);
             }
         }
     };
@@ -397,10 +448,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     for (int i = 0; i < D; ++i) {
         Dma d;
         q |= (uint64_t)(uint32_t)p_prepare(i, d) << (E_BITS * i);
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-            if (j < d.n)
-                dma_issue(d, j);
+        dma_all(d);
     }
 
     // LDS read addresses of this lane (slot 0; token half u = 1 is +2048 bytes)
@@ -475,16 +523,16 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // the first half step's operands are read ahead of the loop.
     __builtin_amdgcn_s_waitcnt(0);
     barrier_step();
-    init_acc(c_slot);
     Ops r0, r1;
     read_half(r0, 0, 0);
 
-    // Barrier k means, for every wave: the DMA of step k + 1 has landed, and
-    // the slot of step k - 1 is free.
     // first half of step t: the second half's operands are read and the refill
-    // DMA is issued, then (t, k-step 0) goes to the matrix cores
-    auto half_a = [&](int t, int bits, const Dma& dm) {
-        const int bh = (bits >> (4 * wh)) & 15;
+    // DMA (if any) is issued, then (t, k-step 0) goes to the matrix cores
+    auto half_a = [&](int t, int bits, const Dma dm) {
+        int bh = (bits >> (4 * wh)) & 15;
+        // opaque to the compiler: a kept-row test is then one scalar bit test
+        // and branch, not a 64-bit mask kept for the other half step
+        asm volatile("" : "+s"(bh));
         read_half(r1, t, 1);
         dma_all(dm);
 #pragma unroll
@@ -499,7 +547,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // second half of step t: (t, k-step 1) while the first half of step t + 1
     // is read (its DMA landed before step t's barrier)
     auto half_b = [&](int t, int bits) {
-        const int bh = (bits >> (4 * wh)) & 15;
+        int bh = (bits >> (4 * wh)) & 15;
+        asm volatile("" : "+s"(bh));
         read_half(r0, t + 1, 0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
@@ -510,21 +559,59 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             }
         }
     };
-    // ---- epilogue of item ck (GELU, one rounding), run after the barrier that
-    // frees the slot of the item's last step.  Per 32 x 32 tile, lane l holds
-    // token l % 32 and outputs 8 q + 4 h + (0..3); swapping the q-even / q-odd
-    // halves between lanes l and l + 32 leaves each lane 8 consecutive outputs
-    // (16 bytes) of its token.  These pass through this wave's own 4 KB of the
-    // freed slot (the parts its next DMA refills) so that every store writes
-    // 8 whole 128-byte lines of Y: lanes 8 i .. 8 i + 7 hold one token's 64
-    // consecutive outputs.  Streaming (non-temporal) stores keep the output
-    // from evicting X and W from the caches.  NSTORE stores per wave and item.
-    auto epilogue = [&](int sslot) {
+    // ---- epilogue of item ck (GELU, one rounding).  Per 32 x 32 tile, lane l
+    // holds token l % 32 and outputs 8 q + 4 h + (0..3); swapping the q-even /
+    // q-odd halves between lanes l and l + 32 leaves each lane 8 consecutive
+    // outputs (16 bytes) of its token.  pack() does that right after the
+    // item's last step; flush() runs after the next barrier, which frees the
+    // slot of that step: the chunks pass through this wave's own 4 KB of the
+    // slot (the parts its next DMA refills) so that every store writes 8 whole
+    // 128-byte lines of Y (lanes 8 i .. 8 i + 7: one token's 64 consecutive
+    // outputs).  Streaming (non-temporal) stores keep the output from evicting
+    // X and W from the caches.  NSTORE stores per wave and item.
+    v4i pko[2][4][2];  // (token half u, tile row j, p2): outputs 32 j + 16 p2 + 8 h + 0..7
+    int64_t f_mw = 0, f_nw = 0;  // the packed item's first token and output of this wave
+    bool f_inside = true;        // ... and whether its whole tile lies inside Y
+    auto pack = [&]() {
         const v4i cd = lds_read16<0>(desc_lds + c_slot * 16);
         const int c_g = __builtin_amdgcn_readfirstlane(cd.x);
-        const int64_t mw = (int64_t)c_mt * BM + wm * 64;        // wave's first token
-        const int64_t nw = (int64_t)c_g * G * TILE + wh * 128;   // wave's first output
-        const bool inside = (int64_t)c_mt * BM + BM <= a.M && (int64_t)(c_g + 1) * G * TILE <= a.N;
+        f_mw = (int64_t)c_mt * BM + wm * 64;
+        f_nw = (int64_t)c_g * G * TILE + wh * 128;
+        f_inside = (int64_t)c_mt * BM + BM <= a.M && (int64_t)(c_g + 1) * G * TILE <= a.N;
+#pragma unroll
+        for (int u = 0; u < 2; ++u) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                uint32_t pk[4][2];
+#pragma unroll
+                for (int qq = 0; qq < 4; ++qq) {
+                    float v[4] = {acc[u][j][4 * qq], acc[u][j][4 * qq + 1], acc[u][j][4 * qq + 2],
+                                  acc[u][j][4 * qq + 3]};
+                    if (GELU) {
+#pragma unroll
+                        for (int x = 0; x < 4; ++x)
+                            v[x] = gelu_erf(v[x]);
+                    }
+                    pk[qq][0] = pack2<DT>(v[0], v[1]);
+                    pk[qq][1] = pack2<DT>(v[2], v[3]);
+                }
+#pragma unroll
+                for (int p2 = 0; p2 < 2; ++p2) {
+                    // lanes < 32 keep q = 2 p2 and take it from lane + 32; lanes
+                    // >= 32 keep q = 2 p2 + 1 and take it from lane - 32
+                    const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * p2][0], pk[2 * p2 + 1][0], false, false);
+                    const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * p2][1], pk[2 * p2 + 1][1], false, false);
+                    pko[u][j][p2].x = (int)s0[0];
+                    pko[u][j][p2].y = (int)s1[0];
+                    pko[u][j][p2].z = (int)s0[1];
+                    pko[u][j][p2].w = (int)s1[1];
+                }
+            }
+        }
+    };
+    auto flush = [&](int sslot) {
+        const int64_t mw = f_mw, nw = f_nw;
+        const bool inside = f_inside;
         // staging: token tau (0..31) of a round at region tau / 16 (X part,
         // then W part of this wave's DMA area), row tau % 16 of 128 bytes,
         // 16-byte chunk k at k ^ ((tau / 2) % 8): conflict-free both ways
@@ -533,99 +620,95 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         const int b = lane & 31;
         const uint32_t wbase = (b < 16 ? st0 : st1) + (b & 15) * 128;
         const int wswz = (b >> 1) & 7;
+        // four rounds (u, lam): tokens 32 u + 0..31, outputs 64 lam + 0..63;
+        // a round's writes follow the previous round's reads (LDS keeps one
+        // wave's accesses in order)
+        v4i o[2][2][4];
 #pragma unroll
         for (int u = 0; u < 2; ++u) {
 #pragma unroll
             for (int lam = 0; lam < 2; ++lam) {
-                // round (u, lam): tokens 32 u + 0..31, outputs 64 lam + 0..63
 #pragma unroll
-                for (int jj = 0; jj < 2; ++jj) {
-                    const int j = 2 * lam + jj;
-                    uint32_t pk[4][2];
-#pragma unroll
-                    for (int qq = 0; qq < 4; ++qq) {
-                        float v[4] = {acc[u][j][4 * qq], acc[u][j][4 * qq + 1], acc[u][j][4 * qq + 2],
-                                      acc[u][j][4 * qq + 3]};
-                        if (GELU) {
-#pragma unroll
-                            for (int x = 0; x < 4; ++x)
-                                v[x] = gelu_erf(v[x]);
-                        }
-                        pk[qq][0] = pack2<DT>(v[0], v[1]);
-                        pk[qq][1] = pack2<DT>(v[2], v[3]);
-                    }
+                for (int jj = 0; jj < 2; ++jj)
 #pragma unroll
                     for (int p2 = 0; p2 < 2; ++p2) {
-                        // lanes < 32 keep q = 2 p2 and take it from lane + 32; lanes
-                        // >= 32 keep q = 2 p2 + 1 and take it from lane - 32
-                        const auto s0 = __builtin_amdgcn_permlane32_swap(pk[2 * p2][0], pk[2 * p2 + 1][0], false, false);
-                        const auto s1 = __builtin_amdgcn_permlane32_swap(pk[2 * p2][1], pk[2 * p2 + 1][1], false, false);
-                        v4i o;
-                        o.x = (int)s0[0];
-                        o.y = (int)s1[0];
-                        o.z = (int)s0[1];
-                        o.w = (int)s1[1];
                         const int k = jj * 4 + 2 * p2 + h;  // chunk of the 128-byte line
-                        lds_write16(wbase + ((k ^ wswz) * 16), o);
+                        lds_write16(wbase + ((k ^ wswz) * 16), pko[u][2 * lam + jj][p2]);
                     }
-                }
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     const int tau = 8 * i + (lane >> 3), k = lane & 7;
-                    const v4i o = lds_read16<0>((i < 2 ? st0 : st1) + (tau & 15) * 128 +
-                                                ((k ^ ((tau >> 1) & 7)) * 16));
+                    o[u][lam][i] = lds_read16<0>((i < 2 ? st0 : st1) + (tau & 15) * 128 +
+                                                 ((k ^ ((tau >> 1) & 7)) * 16));
+                }
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < 2; ++u)
+#pragma unroll
+            for (int lam = 0; lam < 2; ++lam)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const int tau = 8 * i + (lane >> 3), k = lane & 7;
                     const int64_t m = mw + 32 * u + tau, n = nw + 64 * lam + 8 * k;
                     v4i* dst = (v4i*)(Y + (m * a.ldy + n) * 2);
                     if (!inside && !(m < a.M && n < a.N))
                         dst = (v4i*)&g_sink[lane];
-                    __builtin_nontemporal_store(o, dst);
+                    __builtin_nontemporal_store(o[u][lam][i], dst);
                 }
-            }
-        }
     };
 
     // wait until this wave's DMA of step k + 1 has landed (entry: the step
-    // after it, whose DMA may stay in flight), then barrier k.  Allowed in
-    // flight: the last 2 DMA instructions of that later step (its X; any W
-    // instructions come after them, so this may wait a little longer than
-    // needed) and, for the barrier after an item's stores were issued behind
-    // this wave's DMA of step k + 1, those stores.
+    // after it, whose DMA instructions -- this wave's exact count -- may stay
+    // in flight), then barrier k.  For the barrier after an item's stores were
+    // issued behind this wave's DMA of step k + 1, those may stay in flight too.
     auto sync = [&](int entry) {
-        // case = (stores may be in flight) * 2 + (that later step is real)
-        const int cs = (sp > 0 ? 2 : 0) + ((entry >> 9) & 1);
+        int k = 0;  // DMA instruction pairs of the later step
+        if (entry & E_VALID)
+            k = DENSE ? 2 : 1 + ((entry >> wave) & 1);
+        const int cs = (sp > 0 ? 3 : 0) + k;
         sp = sp > 0 ? sp - 1 : 0;
-        if (DENSE)
-            step_barrier_wait<4>(cs);
-        else
-            step_barrier_wait<2>(cs);
+        step_barrier_wait(cs);
     };
-    bool item_done = false;  // the previous step was its item's last
-    for (int t = 0;; ++t) {
-        const int e0 = (int)(q & E_MASK);
-        Dma dx;
-        // barrier t; DMA of step t + 3 into the slot of step t - 1
-        sync((int)((q >> (2 * E_BITS)) & E_MASK));
-        if (item_done) {
-            // the stores go out before this step's DMA: the next barrier lets
-            // them stay in flight, the one after waits for them
-            epilogue((t - 1) & (NS - 1));
-            if (++ck >= my_items)
+    // Barrier k: every wave has read the slot of step k - 1 and waited for its
+    // DMA of step k + 1; after it, each wave issues its DMA of step k + 3 into
+    // the slot of step k - 1.
+    int t = 0;
+    sync((int)((q >> (2 * E_BITS)) & E_MASK));  // barrier 0
+    // One item per iteration.  After its last step: pack(), the barrier that
+    // frees that step's slot, the stores (flush), then the accumulators of the
+    // next item (they are dead from pack() to init_acc()).
+    for (;;) {
+        init_acc(c_slot);
+        bool first = true;
+        for (;;) {
+            const int e0 = (int)(q & E_MASK);
+            Dma d;
+            if (!first)
+                sync((int)((q >> (2 * E_BITS)) & E_MASK));
+            q |= (uint64_t)(uint32_t)p_prepare((t + D) & (NS - 1), d) << (D * E_BITS);
+            half_a(t, e0 & 0xff, d);
+            half_b(t, e0 & 0xff);
+            first = false;
+            q >>= E_BITS;
+            ++t;
+            if (e0 & E_LAST)
                 break;
-            sp = 1;
-            c_slot += a.p_mod;
-            c_mt += a.p_div;
-            if (c_slot >= a.n_slots) {
-                c_slot -= a.n_slots;
-                ++c_mt;
-            }
-            init_acc(c_slot);
-            item_done = false;
         }
-        q |= (uint64_t)(uint32_t)p_prepare((t + D) & (NS - 1), dx) << (3 * E_BITS);
-        half_a(t, e0 & 0xff, dx);
-        half_b(t, e0 & 0xff);
-        item_done = (e0 & E_LAST) != 0;
-        q >>= E_BITS;
+        pack();
+        sync((int)((q >> (2 * E_BITS)) & E_MASK));
+        // the stores go out before the next DMA: the next barrier lets them
+        // stay in flight, the one after waits for them
+        flush((t - 1) & (NS - 1));
+        sp = 1;
+        if (++ck >= my_items)
+            break;
+        c_slot += a.p_mod;
+        c_mt += a.p_div;
+        if (c_slot >= a.n_slots) {
+            c_slot -= a.n_slots;
+            ++c_mt;
+        }
     }
     // no DMA or store of this workgroup may be in flight when it ends
     __builtin_amdgcn_s_waitcnt(0);
