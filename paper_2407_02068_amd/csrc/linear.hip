@@ -54,11 +54,11 @@ namespace {
 constexpr int NT = 512;             // threads per workgroup: 8 waves
 constexpr int G = GROUP_TILES;      // tile rows per item
 constexpr int NS = 4;               // LDS ring slots
-constexpr int D = NS - 1;           // DMA runs D steps ahead of the matrix cores
+// Steps go in pairs, one barrier per pair: after the barrier of pair (b, b + 1)
+// each wave loads steps b + 2 and b + 3 into the slots of b - 2 and b - 1.
 constexpr int XU4 = BM * 4;         // 16-byte chunks of one X slice (256 x 32 elements)
 constexpr int WU4 = G * 128;        // 16-byte chunks of G W tiles (32 x 32 elements each)
 constexpr int SLOT = XU4 + WU4;     // one ring slot: 32 KB
-constexpr int NSTORE = 16;          // store instructions per wave per item
 constexpr int TAB_U4 = 2048;        // per-call tables (walk, slot descriptors, bias): 32 KB
 
 static_assert(XU4 == 2 * 8 * 64 && WU4 == 2 * 8 * 64, "2 X and up to 2 W DMA instructions per wave");
@@ -131,54 +131,6 @@ template <int N> __device__ inline void wait_vm()
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-// The wait before a step barrier and the barrier, as one small branch tree
-// (the compiler spends several times the instructions on it).  Case 3 s + k:
-// this wave's last NSTORE * s + 2 k vector-memory instructions may stay in
-// flight (s: an item's stores, k: 0..2 pairs of DMA instructions).
-__device__ inline void step_barrier_wait(int cs)
-{
-    static_assert(NSTORE == 16, "vmcnt immediates below");
-    asm volatile(
-        "s_cmp_lt_u32 %0, 3\n"
-        "s_cbranch_scc1 1f\n"
-        "s_cmp_eq_u32 %0, 3\n"
-        "s_cbranch_scc1 3f\n"
-        "s_cmp_eq_u32 %0, 4\n"
-        "s_cbranch_scc1 4f\n"
-        "s_waitcnt vmcnt(20)\n"
-        "s_branch 7f\n"
-        "4:\n"
-        "s_waitcnt vmcnt(18)\n"
-        "s_branch 7f\n"
-        "3:\n"
-        "s_waitcnt vmcnt(16)\n"
-        "s_branch 7f\n"
-        "1:\n"
-        "s_cmp_eq_u32 %0, 0\n"
-        "s_cbranch_scc1 5f\n"
-        "s_cmp_eq_u32 %0, 1\n"
-        "s_cbranch_scc1 6f\n"
-        "s_waitcnt vmcnt(4)\n"
-        "s_branch 7f\n"
-        "6:\n"
-        "s_waitcnt vmcnt(2)\n"
-        "s_branch 7f\n"
-        "5:\n"
-        "s_waitcnt vmcnt(0)\n"
-        "7:\n"
-        "s_barrier"
-        :
-        : "s"(cs)
-        : "memory", "scc");
-}
-
-__device__ inline void barrier_step()
-{
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    __builtin_amdgcn_s_barrier();
-    __atomic_signal_fence(__ATOMIC_SEQ_CST);
-}
-
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 // 16-byte LDS read at a byte address (an ordinary load: the compiler places
@@ -246,7 +198,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     for (int i = tid; i < a.n_slots; i += NT) {
         int4 d;
         if (DENSE) {
-            d = make_int4(a.gs0 + i, i * ncol, ncol, 0);
+            const int nw = (ncol + 1) & ~1;  // an even walk: a step with no tile pads it
+            d = make_int4(a.gs0 + i, i * nw, nw, 0);
         } else {
             d = gdesc[a.gs0 + i];
             d.y -= a.walk0;
@@ -265,7 +218,9 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             int col = (int)((int64_t)(a.gs0 + slot) * ncol / a.n_groups) + j;
             if (col >= ncol)
                 col -= ncol;
-            e = make_int2(col | (rows_of(d.x) << 16) | (j == ncol - 1 ? W_LAST : 0), 0);
+            e = make_int2(j < ncol ? col | (rows_of(d.x) << 16) : 0, 0);
+            if (j == d.z - 1)
+                e.x |= W_LAST;
         } else {
             e = walk[a.walk0 + i];
         }
@@ -367,9 +322,10 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         const int col = ex & 0xffff, bits = (ex >> 16) & 0xff;
         d.col = col;
         d.xcol = (uint32_t)col * (TILE * 2);
-        d.n = 2;
+        d.n = bits ? 2 : 0;  // a step that keeps no tile (walk padding) loads nothing
         if (DENSE) {
-            d.n = 4;
+            if (bits)
+                d.n = 4;
         } else if ((bits >> wave) & 1) {  // row `wave` of the group is kept: its tile
             // (the stream holds fewer than 2^21 tiles: the offset fits 32 bits)
             const int rank = __popc(bits & ((1 << wave) - 1));
@@ -442,10 +398,10 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         }
     };
 
-    // ---- prologue: the first D steps
+    // ---- prologue: the first pair of steps
     uint64_t q = 0;  // queue entries of steps t, t + 1, ... (E_BITS each)
 #pragma unroll
-    for (int i = 0; i < D; ++i) {
+    for (int i = 0; i < 2; ++i) {
         Dma d;
         q |= (uint64_t)(uint32_t)p_prepare(i, d) << (E_BITS * i);
         dma_all(d);
@@ -495,7 +451,6 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     int ck = 0;
     int c_mt = item_off / a.n_slots;
     int c_slot = item_off - c_mt * a.n_slots;
-    int sp = 0;  // barriers still to pass while an item's stores may be in flight
 
     // Accumulators start at the bias of their outputs: lane l, register 4 qq
     // + i of tile row j holds output 8 qq + 4 (l / 32) + i of that row.
@@ -519,22 +474,16 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         }
     };
 
-    // Steps 0 .. D - 1 have landed everywhere before anyone reads step 0;
-    // the first half step's operands are read ahead of the loop.
-    __builtin_amdgcn_s_waitcnt(0);
-    barrier_step();
     Ops r0, r1;
-    read_half(r0, 0, 0);
 
-    // first half of step t: the second half's operands are read and the refill
-    // DMA (if any) is issued, then (t, k-step 0) goes to the matrix cores
-    auto half_a = [&](int t, int bits, const Dma dm) {
+    // first half of step t: the second half's operands are read, then (t,
+    // k-step 0) goes to the matrix cores
+    auto half_a = [&](int t, int bits) {
         int bh = (bits >> (4 * wh)) & 15;
         // opaque to the compiler: a kept-row test is then one scalar bit test
         // and branch, not a 64-bit mask kept for the other half step
         asm volatile("" : "+s"(bh));
         read_half(r1, t, 1);
-        dma_all(dm);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (bh & (1 << j)) {
@@ -544,12 +493,13 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             }
         }
     };
-    // second half of step t: (t, k-step 1) while the first half of step t + 1
-    // is read (its DMA landed before step t's barrier)
-    auto half_b = [&](int t, int bits) {
+    // second half of step t: (t, k-step 1), while the first half of step t + 1
+    // is read if it belongs to the same pair
+    auto half_b = [&](int t, int bits, bool pre) {
         int bh = (bits >> (4 * wh)) & 15;
         asm volatile("" : "+s"(bh));
-        read_half(r0, t + 1, 0);
+        if (pre)
+            read_half(r0, t + 1, 0);
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             if (bh & (1 << j)) {
@@ -568,7 +518,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // slot (the parts its next DMA refills) so that every store writes 8 whole
     // 128-byte lines of Y (lanes 8 i .. 8 i + 7: one token's 64 consecutive
     // outputs).  Streaming (non-temporal) stores keep the output from evicting
-    // X and W from the caches.  NSTORE stores per wave and item.
+    // X and W from the caches.  16 stores per wave and item.
     v4i pko[2][4][2];  // (token half u, tile row j, p2): outputs 32 j + 16 p2 + 8 h + 0..7
     int64_t f_mw = 0, f_nw = 0;  // the packed item's first token and output of this wave
     bool f_inside = true;        // ... and whether its whole tile lies inside Y
@@ -658,49 +608,48 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                 }
     };
 
-    // wait until this wave's DMA of step k + 1 has landed (entry: the step
-    // after it, whose DMA instructions -- this wave's exact count -- may stay
-    // in flight), then barrier k.  For the barrier after an item's stores were
-    // issued behind this wave's DMA of step k + 1, those may stay in flight too.
-    auto sync = [&](int entry) {
-        int k = 0;  // DMA instruction pairs of the later step
-        if (entry & E_VALID)
-            k = DENSE ? 2 : 1 + ((entry >> wave) & 1);
-        const int cs = (sp > 0 ? 3 : 0) + k;
-        sp = sp > 0 ? sp - 1 : 0;
-        step_barrier_wait(cs);
-    };
-    // Barrier k: every wave has read the slot of step k - 1 and waited for its
-    // DMA of step k + 1; after it, each wave issues its DMA of step k + 3 into
-    // the slot of step k - 1.
+    // Barrier of pair (b, b + 1): every wave has waited for all of its DMA
+    // (steps b and b + 1, and its stores) and finished with steps b - 2 and
+    // b - 1; their slots are free afterwards.
+    auto sync = [&]() { asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory"); };
     int t = 0;
-    sync((int)((q >> (2 * E_BITS)) & E_MASK));  // barrier 0
-    // One item per iteration.  After its last step: pack(), the barrier that
-    // frees that step's slot, the stores (flush), then the accumulators of the
-    // next item (they are dead from pack() to init_acc()).
+    // prepare and issue the DMA of step t + ahead (steps are prepared in order)
+    auto load = [&](int ahead) {
+        Dma d;
+        q |= (uint64_t)(uint32_t)p_prepare((t + ahead) & (NS - 1), d) << (ahead * E_BITS);
+        dma_all(d);
+    };
+    sync();  // the first pair has landed
+    // One item per iteration (items have an even number of steps).  After its
+    // last pair: pack(), the next barrier (which frees the slots of that
+    // pair), the stores through the slot of the last step (flush), then the
+    // DMA into that slot and the next item's accumulators.  The packed
+    // outputs and the accumulators are never live together.
+    bool have = false;  // pko holds an item not yet stored
     for (;;) {
+        read_half(r0, t, 0);
+        load(2);  // into the slot of step t - 2
+        if (have)
+            flush((t - 1) & (NS - 1));
+        load(3);  // into the slot of step t - 1, after the stores left it
         init_acc(c_slot);
-        bool first = true;
-        for (;;) {
-            const int e0 = (int)(q & E_MASK);
-            Dma d;
-            if (!first)
-                sync((int)((q >> (2 * E_BITS)) & E_MASK));
-            q |= (uint64_t)(uint32_t)p_prepare((t + D) & (NS - 1), d) << (D * E_BITS);
-            half_a(t, e0 & 0xff, d);
-            half_b(t, e0 & 0xff);
-            first = false;
-            q >>= E_BITS;
-            ++t;
-            if (e0 & E_LAST)
+        for (;;) {  // the pairs of the item
+            const int e0 = (int)(q & E_MASK), e1 = (int)((q >> E_BITS) & E_MASK);
+            half_a(t, e0 & 0xff);
+            half_b(t, e0 & 0xff, true);
+            half_a(t + 1, e1 & 0xff);
+            half_b(t + 1, e1 & 0xff, false);
+            q >>= 2 * E_BITS;
+            t += 2;
+            sync();
+            if (e1 & E_LAST)
                 break;
+            read_half(r0, t, 0);
+            load(2);
+            load(3);
         }
         pack();
-        sync((int)((q >> (2 * E_BITS)) & E_MASK));
-        // the stores go out before the next DMA: the next barrier lets them
-        // stay in flight, the one after waits for them
-        flush((t - 1) & (NS - 1));
-        sp = 1;
+        have = true;
         if (++ck >= my_items)
             break;
         c_slot += a.p_mod;
@@ -710,6 +659,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             ++c_mt;
         }
     }
+    flush((t - 1) & (NS - 1));
     // no DMA or store of this workgroup may be in flight when it ends
     __builtin_amdgcn_s_waitcnt(0);
 }
@@ -793,13 +743,13 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
     const int64_t n_mt = (a.d.M + BM - 1) / BM;
     const bool ktail = (a.d.K % TILE) != 0;
     const int P0 = max(num_cus() & ~7, 8);
-    // Launches over consecutive launch slots whose tables fit the 16 KB of LDS
+    // Launches over consecutive launch slots whose tables fit the 32 KB of LDS
     // reserved for them: 16 B per slot descriptor and walk entry, 1 KB of float32 bias
     // per slot.
     for (int gs0 = 0; gs0 < a.d.n_groups;) {
         int ns = 0, nw = 0;
         while (gs0 + ns < a.d.n_groups) {
-            const int len = DENSE ? a.d.n_tile_cols : a.gdesc_host[gs0 + ns].z;
+            const int len = DENSE ? (a.d.n_tile_cols + 1) & ~1 : a.gdesc_host[gs0 + ns].z;
             if ((ns + 1) * (16 + G * TILE * 4) + (nw + len) * 16 > TAB_U4 * 16)
                 break;
             ++ns;

@@ -143,10 +143,11 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_pack_plan(PackArgs a, int32_t*
         }
         group_order[rank] = g;
         s_rank[g] = rank;
-        // steps walked for launch slot `rank`: an empty group still produces
-        // its bias, as one step with no tile
+        // steps walked for launch slot `rank`, padded to an even count (the
+        // kernel takes steps in pairs) with steps that keep no tile; an empty
+        // group still produces its bias, from two such steps
         const int ns = (g + 1 < a.n_groups ? s_gsteps[g + 1] : n_steps) - s_gsteps[g];
-        s_walk[rank] = max(ns, 1);
+        s_walk[rank] = (max(ns, 1) + 1) & ~1;
     }
     __syncthreads();
     // the launch slots' walks lie one after the other, in launch order
@@ -157,7 +158,7 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_pack_plan(PackArgs a, int32_t*
         // the walk of slot `rank` starts at column step rank * ns / n_groups and
         // wraps: slots that run side by side on one token tile read different X
         // columns at a time
-        gdesc[rank] = make_int4(g, s_walk[rank], max(ns, 1),
+        gdesc[rank] = make_int4(g, s_walk[rank], (max(ns, 1) + 1) & ~1,
                                 ns > 0 ? (int)((int64_t)rank * ns / a.n_groups) : 0);
     }
     if (tid == 0) {
@@ -286,8 +287,8 @@ __global__ __launch_bounds__(256) void k_stream_fill(PackArgs a, const int32_t* 
 }
 
 // One wave per launch slot: the slot's walk, the group's steps starting at its
-// rotation and wrapping, as {col | bits << 16 | last << 24, first tile}.  An
-// empty group walks one step with no tile.
+// rotation and wrapping, as {col | bits << 16 | last << 24, first tile}, then
+// steps with no tile up to the (even) walk length.
 __global__ __launch_bounds__(64) void k_walk_fill(const int4* __restrict__ gdesc,
                                                   const int32_t* __restrict__ step_ptr,
                                                   const int32_t* __restrict__ step_col,
@@ -300,7 +301,7 @@ __global__ __launch_bounds__(64) void k_walk_fill(const int4* __restrict__ gdesc
     for (int i = threadIdx.x; i < d.z; i += 64) {
         const int last = (i == d.z - 1) ? 1 << 24 : 0;
         int2 e = make_int2(last, 0);
-        if (ns > 0) {
+        if (i < ns) {
             int j = d.w + i;
             if (j >= ns)
                 j -= ns;
