@@ -46,6 +46,12 @@ class Oracle:
         lib.lpvo_linear.argtypes = [i32, vp, i64, i64, vp, i64, i64, i64, i32, i32, vp, vp,
                                     i32, vp, i64, i32]
         lib.lpvo_linear.restype = i32
+        lib.lpvo_block_scores.argtypes = [i32, vp, i64, vp, i64, i64, i64, i32, i32, vp]
+        lib.lpvo_block_scores.restype = i32
+        lib.lpvo_keep_count.argtypes = [i64, i32]
+        lib.lpvo_keep_count.restype = i64
+        lib.lpvo_mask_topk.argtypes = [vp, i64, i64, vp]
+        lib.lpvo_mask_topk.restype = i32
         self.lib = lib
         self.path = path
 
@@ -130,6 +136,50 @@ class Oracle:
         return Y
 
 
+    def block_scores(self, W, dtype, b_r, b_c, G=None):
+        """Block scores, float64 R x C: the mean of |W * G| per block (the
+        paper's average-pooled Taylor score, Sec. 3.1), or without G the sum of
+        squares per block."""
+        W = np.ascontiguousarray(W)
+        _check(W, dtype, "W")
+        N, K = W.shape
+        if G is not None:
+            G = np.ascontiguousarray(G)
+            _check(G, dtype, "G")
+            if G.shape != W.shape:
+                raise ValueError("G shape %s, expected %s" % (G.shape, W.shape))
+        if b_r <= 0 or b_c <= 0 or N % b_r or K % b_c:
+            raise ValueError("block %dx%d does not divide weight %dx%d" % (b_r, b_c, N, K))
+        out = np.empty((N // b_r, K // b_c), np.float64)
+        if self.lib.lpvo_block_scores(_CODES[dtype], _ptr(W), K, _ptr(G), K, N, K, b_r, b_c,
+                                      _ptr(out)):
+            raise ValueError("lpvo_block_scores rejected its arguments")
+        return out
+
+    def keep_count(self, n_blocks, sparsity_pct):
+        """Kept blocks at an integer sparsity percentage (ceiling rule, Sec. 3.4)."""
+        n = self.lib.lpvo_keep_count(int(n_blocks), int(sparsity_pct))
+        if n < 0:
+            raise ValueError("bad block count or sparsity")
+        return int(n)
+
+    def mask_topk(self, scores, n_keep):
+        """uint8 mask (scores' shape) of the n_keep best-ranked blocks: higher
+        score first, equal scores by lower row-major index."""
+        scores = np.ascontiguousarray(scores, dtype=np.float64)
+        mask = np.empty(scores.shape, np.uint8)
+        rc = self.lib.lpvo_mask_topk(_ptr(scores), scores.size, int(n_keep), _ptr(mask))
+        if rc:
+            raise ValueError("lpvo_mask_topk failed (%d)" % rc)
+        return mask
+
+    def block_mask(self, W, dtype, b_r, b_c, sparsity_pct, G=None):
+        """The pruning mask of Sec. 3.1: scores, then the top ceil((1 - alpha)
+        R C) blocks."""
+        s = self.block_scores(W, dtype, b_r, b_c, G)
+        return self.mask_topk(s, self.keep_count(s.size, sparsity_pct)), s
+
+
 def _ptr(a):
     return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
 
@@ -181,6 +231,22 @@ def unpack(row_ptr, col_idx, values, dtype, N, K, b_r, b_c):
 
 def linear(X, W, dtype, b_r, b_c, mask, bias=None, gelu=False, nthreads=None):
     return default().linear(X, W, dtype, b_r, b_c, mask, bias, gelu, nthreads)
+
+
+def block_scores(W, dtype, b_r, b_c, G=None):
+    return default().block_scores(W, dtype, b_r, b_c, G)
+
+
+def keep_count(n_blocks, sparsity_pct):
+    return default().keep_count(n_blocks, sparsity_pct)
+
+
+def mask_topk(scores, n_keep):
+    return default().mask_topk(scores, n_keep)
+
+
+def block_mask(W, dtype, b_r, b_c, sparsity_pct, G=None):
+    return default().block_mask(W, dtype, b_r, b_c, sparsity_pct, G)
 
 
 def rel_err(y, ref):

@@ -309,3 +309,96 @@ out:
     free(b);
     return rc;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Block scores and the top-k block mask (Sec. 3.1, Sec. 3.4)                */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The paper ranks the blocks of a weight by the 2-D average pool of the
+ * first-order Taylor score of its elements, S = |W . grad_W f| (element-wise),
+ * and drops the bottom-ranked ones for a pruning ratio alpha; the number of
+ * blocks that survive is the ceiling of (1 - alpha) times the block count (the
+ * block term of the power model, Sec. 3.4).
+ *
+ * Score of block (r, c), in float64, its elements visited row by row
+ * (n = r b_r .. r b_r + b_r - 1, and within a row k = c b_c .. c b_c + b_c - 1)
+ * and accumulated one after the other:
+ *   G given:  S'[r][c] = (sum |W[n][k] * G[n][k]|) / (b_r b_c)
+ *   G NULL:   S'[r][c] = sum W[n][k]^2   (no gradient: the block's squared L2
+ *             norm, which ranks blocks like their L2 norm)
+ * Every product of two decoded elements is exact in float64 (at most 24 + 24
+ * significant bits) and b_r b_c is a power of two, so the result depends only
+ * on the fixed summation order.
+ */
+int lpvo_block_scores(int dtype, const void* W, int64_t ldw, const void* G, int64_t ldg,
+                      int64_t N, int64_t K, int b_r, int b_c, double* scores)
+{
+    if (!lpvo_elem_size(dtype) || !grid_ok(N, K, b_r, b_c) || ldw < K || (G && ldg < K) ||
+        ((N > 0 && K > 0) && (!W || !scores)))
+        return -1;
+    const int64_t R = N / b_r, C = K / b_c;
+    for (int64_t r = 0; r < R; ++r) {
+        for (int64_t c = 0; c < C; ++c) {
+            double s = 0.0;
+            for (int64_t n = r * b_r; n < (r + 1) * b_r; ++n) {
+                for (int64_t k = c * b_c; k < (c + 1) * b_c; ++k) {
+                    const double w = dec_one(dtype, W, n * ldw + k);
+                    if (G)
+                        s += fabs(w * dec_one(dtype, G, n * ldg + k));
+                    else
+                        s += w * w;
+                }
+            }
+            scores[r * C + c] = G ? s / (double)(b_r * b_c) : s;
+        }
+    }
+    return 0;
+}
+
+/* ceil((100 - p) / 100 * n_blocks) for an integer percentage p, exactly. */
+int64_t lpvo_keep_count(int64_t n_blocks, int sparsity_pct)
+{
+    if (n_blocks < 0 || sparsity_pct < 0 || sparsity_pct > 100)
+        return -1;
+    return ((100 - (int64_t)sparsity_pct) * n_blocks + 99) / 100;
+}
+
+/* Block i ranks before block j if its score is larger, or the scores are
+ * equal and i is the lower row-major index. */
+static const double* g_rank_scores;
+
+static int rank_cmp(const void* a, const void* b)
+{
+    const int64_t i = *(const int64_t*)a, j = *(const int64_t*)b;
+    const double si = g_rank_scores[i], sj = g_rank_scores[j];
+    if (si > sj)
+        return -1;
+    if (si < sj)
+        return 1;
+    return i < j ? -1 : (i > j ? 1 : 0);
+}
+
+/* mask[i] = 1 for the n_keep best-ranked of n_blocks scores, 0 otherwise.
+ * NaN scores are outside the contract (rejected).  Not thread-safe (qsort
+ * comparator state). */
+int lpvo_mask_topk(const double* scores, int64_t n_blocks, int64_t n_keep, uint8_t* mask)
+{
+    if (n_blocks < 0 || n_keep < 0 || n_keep > n_blocks || (n_blocks > 0 && (!scores || !mask)))
+        return -1;
+    for (int64_t i = 0; i < n_blocks; ++i)
+        if (scores[i] != scores[i])
+            return -1;
+    int64_t* order = (int64_t*)malloc((size_t)(n_blocks > 0 ? n_blocks : 1) * sizeof(int64_t));
+    if (!order)
+        return -2;
+    for (int64_t i = 0; i < n_blocks; ++i)
+        order[i] = i;
+    g_rank_scores = scores;
+    qsort(order, (size_t)n_blocks, sizeof(int64_t), rank_cmp);
+    memset(mask, 0, (size_t)n_blocks);
+    for (int64_t i = 0; i < n_keep; ++i)
+        mask[order[i]] = 1;
+    free(order);
+    return 0;
+}

@@ -46,6 +46,22 @@ int lpvo_linear(int dtype, const void* X, int64_t ldx, int64_t M,
                 int b_r, int b_c, const uint8_t* mask, const void* bias,
                 int gelu, double* Y, int64_t ldy, int nthreads);
 
+/* Block scores (R x C float64, row-major): with G, the mean of |W * G| over
+ * each block (the average-pooled first-order Taylor score); without G (NULL),
+ * the sum of squares of the block's elements.  Elements are visited row by row
+ * within the block and summed one after the other.  Returns 0, or -1 on a bad
+ * argument. */
+int lpvo_block_scores(int dtype, const void* W, int64_t ldw, const void* G, int64_t ldg,
+                      int64_t N, int64_t K, int b_r, int b_c, double* scores);
+
+/* Blocks kept at an integer sparsity percentage: ceil((100 - p) n / 100).
+ * Returns -1 on a bad argument. */
+int64_t lpvo_keep_count(int64_t n_blocks, int sparsity_pct);
+
+/* Mask of the n_keep highest scores (ties: the lower index first).  Returns 0,
+ * -1 on a bad argument (NaN scores included), -2 when host memory runs out. */
+int lpvo_mask_topk(const double* scores, int64_t n_blocks, int64_t n_keep, uint8_t* mask);
+
 #ifdef __cplusplus
 }
 #endif

@@ -9,7 +9,8 @@ with planted mistakes and requires every mistake to be caught.
 Independent references used here: the hand-worked fixture under ``golden/``,
 the standard normal table, ``scipy.sparse.bsr_matrix`` (BSR arrays),
 ``numpy.matmul`` / ``numpy.kron`` (dense products, mask expansion), integer
-arithmetic in int64, torch's CPU bf16 conversion and numpy's float16.
+arithmetic in int64, torch's CPU bf16 conversion and numpy's float16, and
+numpy's reshape-sum and lexsort (block scores, the top-k order).
 """
 import json
 import math
@@ -326,6 +327,78 @@ def pin_rejects_bad_grids(orc):
                              None, None, None) == -1
     assert orc.lib.lpvo_pack(0, W.ctypes.data, 64, 48, 64, 16, 16, m.ctypes.data,
                              None, None, None) == 12
+
+
+# ---- block scores and the top-k mask (Sec. 3.1 ranking, Sec. 3.4 count) ----
+
+def pin_scores_vs_numpy(orc):
+    """Block scores equal numpy's block sums (reshape + sum, its own order)
+    to 1e-12 relative, and exactly for integer-valued weights; the Taylor form
+    is the mean of |W * G| (signs in both W and G)."""
+    g = np.random.default_rng(31)
+    for dtype, N, K, b_r, b_c in (("f32", 64, 96, 16, 32), ("bf16", 96, 64, 32, 16),
+                                  ("f16", 128, 128, 64, 64)):
+        W = wl.quantize(g.standard_normal((N, K)).astype(np.float32), dtype)
+        G = wl.quantize(g.standard_normal((N, K)).astype(np.float32), dtype)
+        w, gg = orc.decode(W, dtype), orc.decode(G, dtype)
+        R, C = N // b_r, K // b_c
+        l2 = (w * w).reshape(R, b_r, C, b_c).sum(axis=(1, 3))
+        ty = np.abs(w * gg).reshape(R, b_r, C, b_c).mean(axis=(1, 3))
+        np.testing.assert_allclose(orc.block_scores(W, dtype, b_r, b_c), l2, rtol=1e-12)
+        np.testing.assert_allclose(orc.block_scores(W, dtype, b_r, b_c, G), ty, rtol=1e-12)
+    Wi = g.integers(-8, 9, (64, 64)).astype(np.float32)
+    Gi = g.integers(-8, 9, (64, 64)).astype(np.float32)
+    l2 = (Wi.astype(np.float64) ** 2).reshape(4, 16, 4, 16).sum(axis=(1, 3))
+    assert np.array_equal(orc.block_scores(Wi, "f32", 16, 16), l2)
+    ty = np.abs(Wi.astype(np.float64) * Gi).reshape(4, 16, 4, 16).sum(axis=(1, 3)) / 256.0
+    assert np.array_equal(orc.block_scores(Wi, "f32", 16, 16, Gi), ty)
+
+
+def pin_scores_onehot_block(orc):
+    """A weight that is zero except in block (r, c) scores zero everywhere but
+    (r, c): the score grid is indexed (row-block, column-block)."""
+    N, K, b_r, b_c = 96, 64, 32, 16
+    for r, c in ((0, 3), (2, 1), (1, 0)):
+        W = np.zeros((N, K), np.float32)
+        W[r * b_r:(r + 1) * b_r, c * b_c:(c + 1) * b_c] = 0.5
+        s = orc.block_scores(W, "f32", b_r, b_c)
+        want = np.zeros((N // b_r, K // b_c))
+        want[r, c] = 0.25 * b_r * b_c
+        assert np.array_equal(s, want), (r, c)
+
+
+def pin_keep_count_ceiling(orc):
+    """ceil((1 - alpha) R C) (Sec. 3.4) at integer percentages."""
+    cases = {(2304, 50): 1152, (2304, 25): 1728, (10, 33): 7, (3, 50): 2, (7, 0): 7,
+             (7, 100): 0, (0, 50): 0, (9216, 90): 922, (576, 90): 58, (100, 1): 99}
+    for (n, p), want in cases.items():
+        assert orc.keep_count(n, p) == want, (n, p)
+
+
+def pin_topk_vs_lexsort(orc):
+    """The mask keeps the first n_keep of numpy's lexsort by (-score, index),
+    for random scores with many exact ties."""
+    g = np.random.default_rng(32)
+    for R, C in ((1, 1), (3, 5), (12, 24), (48, 12)):
+        s = g.integers(0, 6, (R, C)).astype(np.float64) * 0.25
+        for keep in sorted({0, 1, R * C // 2, R * C - 1, R * C}):
+            keep = max(0, keep)
+            order = np.lexsort((np.arange(R * C), -s.reshape(-1)))
+            want = np.zeros(R * C, np.uint8)
+            want[order[:keep]] = 1
+            assert np.array_equal(orc.mask_topk(s, keep).reshape(-1), want), (R, C, keep)
+
+
+def pin_topk_ties_to_lower_index(orc):
+    """Equal scores: the lower row-major indices are kept; strictly decreasing
+    scores keep a prefix; the highest score is always kept."""
+    s = np.full((4, 6), 2.0)
+    m = orc.mask_topk(s, 10).reshape(-1)
+    assert m[:10].all() and not m[10:].any()
+    d = np.arange(24, 0, -1, dtype=np.float64).reshape(4, 6)
+    assert np.array_equal(orc.mask_topk(d, 5).reshape(-1), (np.arange(24) < 5).astype(np.uint8))
+    u = np.arange(24, dtype=np.float64).reshape(4, 6)
+    assert orc.mask_topk(u, 1)[3, 5] == 1 and orc.mask_topk(u, 1).sum() == 1
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

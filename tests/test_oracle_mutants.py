@@ -44,6 +44,20 @@ MUTANTS = {
     "f16_subnormal_scale": ("ldexp((double)f, -24)", "ldexp((double)f, -25)"),
     "f16_exponent_bias": ("ldexp((double)(1024 + f), e - 25)", "ldexp((double)(1024 + f), e - 24)"),
     "bf16_shift": ("uint32_t u = (uint32_t)b << 16;", "uint32_t u = (uint32_t)b << 15;"),
+    "score_abs_dropped": ("s += fabs(w * dec_one(dtype, G, n * ldg + k));",
+                          "s += w * dec_one(dtype, G, n * ldg + k);"),
+    "score_grid_transposed": ("scores[r * C + c] = G ? s / (double)(b_r * b_c) : s;",
+                              "scores[c * R + r] = G ? s / (double)(b_r * b_c) : s;"),
+    "score_last_column_dropped": ("for (int64_t k = c * b_c; k < (c + 1) * b_c; ++k) {",
+                                  "for (int64_t k = c * b_c; k < (c + 1) * b_c - 1; ++k) {"),
+    "score_not_averaged": ("scores[r * C + c] = G ? s / (double)(b_r * b_c) : s;",
+                           "scores[r * C + c] = s;"),
+    "keep_count_floor": ("return ((100 - (int64_t)sparsity_pct) * n_blocks + 99) / 100;",
+                         "return ((100 - (int64_t)sparsity_pct) * n_blocks) / 100;"),
+    "topk_ties_to_higher": ("return i < j ? -1 : (i > j ? 1 : 0);",
+                            "return i < j ? 1 : (i > j ? -1 : 0);"),
+    "topk_keeps_lowest": ("    if (si > sj)\n        return -1;\n    if (si < sj)\n        return 1;",
+                          "    if (si > sj)\n        return 1;\n    if (si < sj)\n        return -1;"),
 }
 
 RUNNER = r"""
