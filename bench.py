@@ -226,6 +226,9 @@ def main():
         log("profile pass done")
         h.close()
         return
+    # the block mask of the same weight on the GPU (scores + top-k), one-time per weight
+    maskgen = lambda: lpv.mask_topk(W, w.b_r, w.b_c, args.sparsity)
+    _, mgms = time_launches(maskgen, 20, 3)
     wall, ms = time_launches(sparse, args.steps, args.warmup)
     dwall, dms = time_launches(dense, args.steps, args.warmup)
     # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
@@ -246,7 +249,8 @@ def main():
         % (pct(ms, .5) * 1e3, pct(ms, .1) * 1e3, pct(ms, .9) * 1e3, achieved, hbm_gbs))
     log("dense_linear: median %.1f us, %.0f TFLOP/s; hipBLASLt addmm median %.1f us"
         % (pct(dms, .5) * 1e3, w.dense_flops() / (dense_avg * 1e-3) / 1e12, pct(bms, .5) * 1e3))
-    log("pack: %.2f ms (one-time)" % pack_ms)
+    log("pack: %.2f ms (one-time); mask_topk median %.1f us (one-time)"
+        % (pack_ms, pct(mgms, .5) * 1e3))
 
     out = {
         "metric": "effective TFLOP/s + speedup vs dense, DeiT-B fc1 at 50% block sparsity",
@@ -274,6 +278,7 @@ def main():
         "bsr_ms_p90": round(pct(ms, .9), 5),
         "hipblaslt_addmm_ms": round(pct(bms, .5), 5),
         "pack_ms": round(pack_ms, 3),
+        "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic,

@@ -176,6 +176,32 @@ lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lp
                             const void* X, int64_t ldx, int64_t M, const void* bias, void* Y,
                             int64_t ldy, lpv_epilogue epi, void* stream);
 
+/*
+ * lpv_mask_topk -- the block mask of a weight (Sec. 3.1): score every b_r x b_c
+ * block, keep the ceil((100 - sparsity_pct) R C / 100) best-ranked (Sec. 3.4's
+ * kept-block count at an integer percentage), drop the rest.
+ *
+ * W       device, N x K, row stride ldw >= K, element type dt.
+ * G       device, N x K (row stride ldg >= K), dt: the loss gradient dL/dW.
+ *         Given, a block's score is the mean of |W * G| over its elements (the
+ *         paper's 2-D average pool of the first-order Taylor score); NULL, it
+ *         is the block's sum of squares W^2 (ranks like the L2 norm).
+ * mask    device, R x C uint8, row-major (R = N / b_r, C = K / b_c): 1 keeps
+ *         the block.  It is the input of lpv_bsr_pack.
+ * scores  device, R x C float64, receives the block scores (also the
+ *         selection's workspace).
+ *
+ * A score is summed in float64 over the block's elements in row-major order,
+ * one addition after the other, so its value is reproducible bit for bit.
+ * Ranking: larger score first, equal scores by lower row-major block index.
+ * NaN in W or G is outside the contract.  Two kernel launches on `stream`, no
+ * allocation, no host synchronisation.  b_r, b_c in {16, 32, 64}.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, BLOCK, HIP.
+ */
+lpv_status lpv_mask_topk(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                         int32_t b_r, int32_t b_c, const void* G, int64_t ldg,
+                         int32_t sparsity_pct, uint8_t* mask, double* scores, void* stream);
+
 /* Release a handle and its device buffers.  NULL-safe.  The caller must make
  * sure no enqueued work still uses it. */
 void lpv_bsr_destroy(lpv_bsr* h);

@@ -398,6 +398,38 @@ lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lp
     return e == hipSuccess ? LPV_OK : hip_fail(e, "dense_linear launch");
 }
 
+lpv_status lpv_mask_topk(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                         int32_t b_r, int32_t b_c, const void* G, int64_t ldg,
+                         int32_t sparsity_pct, uint8_t* mask, double* scores, void* stream)
+{
+    g_err[0] = 0;
+    const int es = elem_size(dt);
+    if (!es)
+        return fail(LPV_ERR_DTYPE, "unknown element type %d", (int)dt);
+    if (check_block(b_r) || check_block(b_c))
+        return fail(LPV_ERR_BLOCK, "block %dx%d: each side must be 16, 32 or 64", b_r, b_c);
+    if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM)
+        return fail(LPV_ERR_SHAPE, "weight %lldx%lld: each side must be in [1, %lld]",
+                    (long long)N, (long long)K, (long long)MAX_DIM);
+    if (N % b_r || K % b_c)
+        return fail(LPV_ERR_SHAPE, "block %dx%d does not divide weight %lldx%lld", b_r, b_c,
+                    (long long)N, (long long)K);
+    if (sparsity_pct < 0 || sparsity_pct > 100)
+        return fail(LPV_ERR_INVALID_ARG, "sparsity %d%% is outside [0, 100]", sparsity_pct);
+    if (!W || !mask || !scores)
+        return fail(LPV_ERR_INVALID_ARG, "W, mask and scores must not be NULL");
+    if (ldw < K || (G && ldg < K))
+        return fail(LPV_ERR_INVALID_ARG, "ldw and ldg must be >= K");
+    if ((uintptr_t)W % es || (G && (uintptr_t)G % es) || (uintptr_t)scores % 8)
+        return fail(LPV_ERR_INVALID_ARG, "W and G must be aligned to their element size, scores "
+                                         "to 8 bytes");
+    const int64_t nb = (N / b_r) * (K / b_c);
+    lpv::MaskCall m = {W, ldw, G, ldg, N, K, (int)dt, b_r, b_c,
+                       ((100 - (int64_t)sparsity_pct) * nb + 99) / 100, mask, scores};
+    hipError_t e = lpv::launch_mask_topk(m, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "mask_topk launch");
+}
+
 void lpv_bsr_destroy(lpv_bsr* h)
 {
     free_handle(h);

@@ -81,4 +81,18 @@ hipError_t launch_bsr_linear(const lpv_bsr* h, const LinearCall& c, hipStream_t 
 hipError_t launch_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, int dtype,
                                const LinearCall& c, hipStream_t s);
 
+// mask.hip
+struct MaskCall {
+    const void* W;
+    int64_t ldw;
+    const void* G;  // NULL: sum-of-squares scores
+    int64_t ldg, N, K;
+    int dtype;
+    int32_t b_r, b_c;
+    int64_t n_keep;
+    uint8_t* mask;
+    double* scores;
+};
+hipError_t launch_mask_topk(const MaskCall& m, hipStream_t s);
+
 }  // namespace lpv

@@ -20,8 +20,8 @@ STATUS = {0: "LPV_OK", -1: "LPV_ERR_INVALID_ARG", -2: "LPV_ERR_SHAPE", -3: "LPV_
 DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 EPI = {None: 0, "none": 0, "gelu": 1}
 EXPORTED = ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
-            "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_bsr_destroy",
-            "lpv_status_str", "lpv_last_error")
+            "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
+            "lpv_bsr_destroy", "lpv_status_str", "lpv_last_error")
 
 
 class LpvError(RuntimeError):
@@ -62,8 +62,9 @@ def lib():
     L.lpv_bsr_unpack.argtypes = [vp, vp, i64, vp]
     L.lpv_bsr_linear.argtypes = [vp, vp, i64, i64, vp, vp, i64, i32, vp]
     L.lpv_dense_linear.argtypes = [vp, i64, i64, i64, i32, vp, i64, i64, vp, vp, i64, i32, vp]
+    L.lpv_mask_topk.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, i32, vp, vp, vp]
     for f in ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
-              "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear"):
+              "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk"):
         getattr(L, f).restype = i32
     L.lpv_bsr_destroy.argtypes = [vp]
     L.lpv_bsr_destroy.restype = None
@@ -253,3 +254,25 @@ def dense_linear(W, X, bias=None, Y=None, epi=None, stream=None):
     _check(lib().lpv_dense_linear(wp, ldw, N, K, DTYPES[W.dtype], xp, ldx, M, _vec(bias, "bias"),
                                   yp, ldy, EPI[epi], _stream(stream)), "lpv_dense_linear")
     return Y
+
+
+def mask_topk(W, b_r, b_c, sparsity_pct, G=None, stream=None):
+    """lpv_mask_topk: block scores of W (mean |W * G| per block, or the block
+    sum of squares without G) and the uint8 mask that keeps the
+    ceil((100 - sparsity_pct) R C / 100) best-ranked blocks.  Returns
+    (mask [R, C] uint8, scores [R, C] float64), both on W's device."""
+    wp, ldw = _mat(W, "W")
+    N, K = W.shape
+    gp, ldg = None, 0
+    if G is not None:
+        if G.dtype != W.dtype or G.shape != W.shape:
+            raise ValueError("G must match W's shape and dtype")
+        gp, ldg = _mat(G, "G")
+    R, C = (N // b_r, K // b_c) if b_r > 0 and b_c > 0 else (0, 0)
+    mask = torch.empty((max(R, 1), max(C, 1)), dtype=torch.uint8, device=W.device)
+    scores = torch.empty((max(R, 1), max(C, 1)), dtype=torch.float64, device=W.device)
+    _check(lib().lpv_mask_topk(wp, ldw, N, K, DTYPES[W.dtype], b_r, b_c, gp, ldg,
+                               int(sparsity_pct), ctypes.c_void_p(mask.data_ptr()),
+                               ctypes.c_void_p(scores.data_ptr()), _stream(stream)),
+           "lpv_mask_topk")
+    return mask, scores

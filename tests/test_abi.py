@@ -125,3 +125,21 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(lpv, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError, match="not built"):
         lpv.lib()
+
+
+def mask_topk(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, b_r=32, b_c=32, G=0, ldg=768, p=50,
+              mask=FAKE + (1 << 32), scores=FAKE + (2 << 32)):
+    return L.lpv_mask_topk(W, ldw, N, K, dt, b_r, b_c, G, ldg, p, mask, scores, None)
+
+
+@pytest.mark.parametrize("kw,want", [
+    (dict(dt=5), DTYPE), (dict(b_r=8), BLOCK), (dict(b_c=24), BLOCK),
+    (dict(N=3072 + 16), SHAPE), (dict(K=0), SHAPE), (dict(N=1 << 17), SHAPE),
+    (dict(p=-1), INVALID), (dict(p=101), INVALID),
+    (dict(W=0), INVALID), (dict(mask=0), INVALID), (dict(scores=0), INVALID),
+    (dict(ldw=700), INVALID), (dict(G=FAKE + (3 << 32), ldg=100), INVALID),
+    (dict(W=FAKE + 1), INVALID), (dict(scores=FAKE + (2 << 32) + 4), INVALID),
+])
+def test_mask_topk_rejects_bad_arguments(L, kw, want):
+    assert mask_topk(L, **kw) == want
+    assert L.lpv_last_error().decode() != ""

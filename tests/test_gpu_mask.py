@@ -1,0 +1,80 @@
+"""GPU parity of lpv_mask_topk against the float64 oracle.
+
+The block scores are specified down to the summation order (float64, row-major
+within a block, one addition after another), so the GPU's scores must equal
+the oracle's bit for bit, and the kept set -- an integer decision taken from
+them -- must be identical.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from gpu_util import dev, say
+from paper_2407_02068_amd import lpv
+
+pytestmark = pytest.mark.gpu
+
+
+def check(W, dtype, b_r, b_c, p, G=None, what=""):
+    say("mask_topk", what, dtype, W.shape, (b_r, b_c), p, "taylor" if G is not None else "l2")
+    m_gpu, s_gpu = lpv.mask_topk(dev(W, dtype), b_r, b_c, p,
+                                 None if G is None else dev(G, dtype))
+    torch.cuda.synchronize()
+    m_ref, s_ref = oracle.block_mask(W, dtype, b_r, b_c, p, G)
+    s = s_gpu.cpu().numpy()
+    assert np.array_equal(s.view(np.uint64), s_ref.view(np.uint64)), "scores differ"
+    m = m_gpu.cpu().numpy()
+    assert np.array_equal(m, m_ref), "masks differ in %d blocks" % int((m != m_ref).sum())
+    assert int(m.sum()) == oracle.keep_count(m.size, p)
+    return m
+
+
+def weights(seed, N, K, dtype, scale=0.02):
+    g = np.random.default_rng(seed)
+    return wl.quantize(g.normal(0, scale, (N, K)).astype(np.float32), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("b_r,b_c", [(16, 16), (32, 32), (64, 32), (16, 64)])
+def test_scores_and_mask_match_oracle(dtype, b_r, b_c):
+    W = weights(61 + b_r + b_c, 384, 256, dtype)
+    G = weights(62 + b_r + b_c, 384, 256, dtype, scale=1.0)
+    for p in (0, 30, 50, 90, 100):
+        check(W, dtype, b_r, b_c, p, what="l2")
+    check(W, dtype, b_r, b_c, 50, G, what="taylor")
+
+
+def test_ties_go_to_the_lower_index():
+    # equal blocks everywhere: the kept set is the first n_keep in row-major order
+    W = np.ones((128, 192), np.float32)
+    m = check(W, "f32", 32, 32, 40, what="all equal")
+    n = oracle.keep_count(m.size, 40)
+    assert m.reshape(-1)[:n].all() and not m.reshape(-1)[n:].any()
+    # integer weights with many equal block sums
+    g = np.random.default_rng(63)
+    Wi = g.integers(-2, 3, (256, 256)).astype(np.float32)
+    check(Wi, "f32", 16, 16, 50, what="integer ties")
+    check(Wi.astype(np.float16), "f16", 16, 16, 75, Wi.astype(np.float16), what="integer taylor")
+
+
+def test_headline_weight():
+    # DeiT-B fc1: 3072 x 768 bf16 at 50%, and the 16x16 grid of the same weight
+    W = wl.b_fc1().W
+    check(W, "bf16", 32, 32, 50, what="b_fc1")
+    check(W, "bf16", 16, 16, 75, what="b_fc1 16x16")
+
+
+def test_mask_feeds_pack_and_linear():
+    # the generated mask drives the hot path: pack it and check the layer
+    w = wl.custom(64, 300, 384, 256, 32, 32, "bf16", "uniform", 50)
+    m_gpu, _ = lpv.mask_topk(dev(w.W, "bf16"), 32, 32, 60)
+    h = lpv.bsr_pack(dev(w.W, "bf16"), m_gpu, 32, 32)
+    Y = lpv.bsr_linear(h, dev(w.X, "bf16"), dev(w.bias, "bf16"))
+    torch.cuda.synchronize()
+    mask, _ = oracle.block_mask(w.W, "bf16", 32, 32, 60)
+    r = oracle.linear(w.X, w.W, "bf16", 32, 32, mask, w.bias)
+    err = oracle.rel_err(Y.float().cpu().numpy().astype(np.float64), r)
+    say("  mask -> pack -> linear rel err %.3e" % err)
+    assert err <= 2e-2
