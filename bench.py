@@ -25,6 +25,8 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16/fp16 matrix-core peak (published)
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bsr_linear_fc1_hbm_traffic.json")
+CLOCK_FILE = os.path.join(ROOT, "profiles", "bsr_linear_fc1_gpu_clock.md")
+STATS_FILE = os.path.join(ROOT, "profiles", "bsr_linear_deit_b_fc1_bf16_kernel_stats.md")
 KERNEL_SOURCES = ("paper_2407_02068_amd/csrc/linear.hip", "paper_2407_02068_amd/csrc/lpv_device.h",
                   "paper_2407_02068_amd/csrc/lpv_internal.h")
 
@@ -60,6 +62,7 @@ def algorithmic_bytes(M, N, K, nnzb, b_r, b_c, kused_cols, es=2):
 
 
 SPARSE_KERNEL = "k_linear16<2, false, false"   # bf16, no GELU, block-sparse (demangled prefix)
+DENSE_KERNEL = "k_linear16<2, false, true"     # bf16, no GELU, dense
 CALIB_BYTES = 1 << 30                        # the calibration copy reads and writes this much
 
 
@@ -103,6 +106,88 @@ def write_traffic(fetch_csv, write_csv, command):
     print(json.dumps(out, indent=1))
 
 
+def kernel_label(name):
+    """A short name for a kernel of the rocprofv3 statistics."""
+    labels = ((SPARSE_KERNEL, "k_linear16 bf16 block-sparse (lpv_bsr_linear)"),
+              (DENSE_KERNEL, "k_linear16 bf16 dense (lpv_dense_linear)"),
+              ("k_block_scores", "k_block_scores (lpv_mask_topk)"),
+              ("k_mask_topk", "k_mask_topk (lpv_mask_topk)"),
+              ("FillFunctor", "torch fill (cache flush between cold launches)"))
+    for key, label in labels:
+        if key in name:
+            return label
+    for key in ("k_pack_plan", "k_pack_compact", "k_sched_fill", "k_stream_fill", "k_walk_fill"):
+        if key in name:
+            return key + " (lpv_bsr_pack)"
+    return name.split("(")[0][:72]
+
+
+def write_stats(stats_csv, command):
+    """The rocprofv3 --kernel-trace --stats summary of a bench.py run as a
+    short table next to the other profiles."""
+    import csv
+    rows = list(csv.DictReader(open(stats_csv)))
+    text = ["# rocprofv3 kernel statistics: DeiT-B fc1 (X 50432 x 768 -> 3072), bf16, 32x32 blocks, "
+            "50% block sparsity", "",
+            "Profiled run, then this summary (from the repository root on one MI355X):", "", "```",
+            "rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
+            "-- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed", command, "```", "",
+            "| kernel | calls | avg us | min us | max us | % of GPU time |",
+            "|---|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        text.append("| %s | %s | %.1f | %.1f | %.1f | %.2f |" % (
+            kernel_label(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
+            float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
+    sp = [r for r in rows if SPARSE_KERNEL in r["Name"]]
+    if sp:
+        avg_us = float(sp[0]["AverageNs"]) / 1e3
+        text += ["", "The hipBLASLt row (Cijk) is `torch.addmm` at the same shape, a check on the "
+                 "dense path.  Kept work of one block-sparse launch: 118.98 GFLOP, so the "
+                 "block-sparse average above is %.0f TFLOP/s (%.1f%% of the 2.5 PFLOP/s bf16 "
+                 "matrix-core peak); `bench.py` times the same launches with HIP events on their "
+                 "stream and reports that average as `roofline.achieved`."
+                 % (118.98e9 / (avg_us * 1e-6) / 1e12, 118.98e9 / (avg_us * 1e-6) / 1e12 / 25.0)]
+    with open(STATS_FILE, "w") as f:
+        f.write("\n".join(text) + "\n")
+    print("\n".join(text))
+
+
+def write_clock(csv_path, command):
+    """The GPU clock achieved during each kernel of a ``--profile-pass`` run:
+    GRBM_GUI_ACTIVE cycles of the dispatch (rocprofv3 sums the counter over
+    the XCDs, so per XCD: divided by their number, from the agent record) over
+    its duration (counter timestamps, ns); written next to the other profiles."""
+    import csv
+    agents = os.path.join(os.path.dirname(csv_path),
+                          os.path.basename(csv_path).replace("counter_collection", "agent_info"))
+    n_xcc = max(int(a.get("Num_Xcc") or 0) for a in csv.DictReader(open(agents)))
+    rows = [r for r in csv.DictReader(open(csv_path)) if r["Counter_Name"] == "GRBM_GUI_ACTIVE"]
+    lines = []
+    for name, key in (("k_linear16 bf16 block-sparse (lpv_bsr_linear)", SPARSE_KERNEL),
+                      ("k_linear16 bf16 dense (lpv_dense_linear)", DENSE_KERNEL)):
+        sel = [r for r in rows if key in r["Kernel_Name"]]
+        if not sel:
+            raise SystemExit("%s: no GRBM_GUI_ACTIVE rows for %s" % (csv_path, key))
+        for r in sel:
+            ns = float(r["End_Timestamp"]) - float(r["Start_Timestamp"])
+            cyc = float(r["Counter_Value"])
+            lines.append("| %s | %s | %.1f | %.0f | %.0f |" % (name, r["Dispatch_Id"], ns / 1e3, cyc,
+                                                               cyc / n_xcc / ns * 1e3))
+    text = ["# GPU clock during the kernels: DeiT-B fc1 (X 50432 x 768 -> 3072), bf16, "
+            "32x32 blocks, 50% block sparsity", "",
+            "Counter run (from the repository root on one MI355X), then this summary:", "", "```",
+            "rocprofv3 --pmc GRBM_GUI_ACTIVE -d gpurun_out/pmc_clock -o clock --output-format csv "
+            "-- python bench.py --profile-pass", command, "```", "",
+            "Each row is one dispatch of the profile pass (three launches of each path, "
+            "serialised by the counter collection): the active cycles, summed over the "
+            "%d XCDs, divided by their number and by the dispatch's duration." % n_xcc, "",
+            "| kernel | dispatch | us | GRBM_GUI_ACTIVE cycles | MHz |",
+            "|---|---:|---:|---:|---:|"] + lines
+    with open(CLOCK_FILE, "w") as f:
+        f.write("\n".join(text) + "\n")
+    print("\n".join(text))
+
+
 def time_launches(fn, steps, warmup):
     import torch
     for _ in range(warmup):
@@ -120,6 +205,22 @@ def time_launches(fn, steps, warmup):
     wall = time.perf_counter() - t0
     ms = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
     return wall, ms
+
+
+def time_flushed(fn, steps, flush_buf):
+    """Each launch timed alone after writing flush_buf (larger than L2 and the
+    256 MB MALL together), so that X, W and Y start outside the caches."""
+    import torch
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(steps)]
+    fn()
+    for i in range(steps):
+        flush_buf.fill_(i & 0x7f)
+        starts[i].record()
+        fn()
+        ends[i].record()
+    torch.cuda.synchronize()
+    return sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
 
 
 def pct(ms, q):
@@ -162,6 +263,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-flushed", action="store_true",
+                    help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
     ap.add_argument("--dtype", default="bf16", choices=["bf16", "f16"])
     ap.add_argument("--block", type=int, default=32)
@@ -170,10 +273,20 @@ def main():
                     help="only 3 launches of each path and a 1 GiB device copy (rocprofv3 counter runs)")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two --profile-pass counter CSVs into the HBM traffic summary")
+    ap.add_argument("--write-stats", metavar="STATS_CSV",
+                    help="turn a rocprofv3 --stats kernel CSV of this script into the statistics summary")
+    ap.add_argument("--write-clock", metavar="CLOCK_CSV",
+                    help="turn a --profile-pass GRBM_GUI_ACTIVE counter CSV into the clock summary")
     args = ap.parse_args()
 
     if args.write_traffic:
         write_traffic(*args.write_traffic, command=" ".join(["python bench.py"] + sys.argv[1:]))
+        return
+    if args.write_stats:
+        write_stats(args.write_stats, command=" ".join(["python bench.py"] + sys.argv[1:]))
+        return
+    if args.write_clock:
+        write_clock(args.write_clock, command=" ".join(["python bench.py"] + sys.argv[1:]))
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -234,6 +347,13 @@ def main():
     # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
     bl = lambda: torch.addmm(b, X, W.t())
     _, bms = time_launches(bl, max(5, args.steps // 2), 3)
+    # cold caches: the same launches after a 1 GiB write each
+    fms = fdms = None
+    if not args.no_flushed:
+        flush_buf = torch.empty(CALIB_BYTES, dtype=torch.uint8, device="cuda")
+        fms = time_flushed(sparse, 20, flush_buf)
+        fdms = time_flushed(dense, 20, flush_buf)
+        del flush_buf
 
     kept_flops = w.kept_flops()
     ms_step = wall / args.steps * 1e3
@@ -249,6 +369,9 @@ def main():
         % (pct(ms, .5) * 1e3, pct(ms, .1) * 1e3, pct(ms, .9) * 1e3, achieved, hbm_gbs))
     log("dense_linear: median %.1f us, %.0f TFLOP/s; hipBLASLt addmm median %.1f us"
         % (pct(dms, .5) * 1e3, w.dense_flops() / (dense_avg * 1e-3) / 1e12, pct(bms, .5) * 1e3))
+    if fms:
+        log("flushed caches: bsr_linear median %.1f us, dense_linear median %.1f us (speedup %.2fx)"
+            % (pct(fms, .5) * 1e3, pct(fdms, .5) * 1e3, pct(fdms, .5) / pct(fms, .5)))
     log("pack: %.2f ms (one-time); mask_topk median %.1f us (one-time)"
         % (pack_ms, pct(mgms, .5) * 1e3))
 
@@ -277,6 +400,11 @@ def main():
         "bsr_ms_p10": round(pct(ms, .1), 5),
         "bsr_ms_p90": round(pct(ms, .9), 5),
         "hipblaslt_addmm_ms": round(pct(bms, .5), 5),
+        "flushed": None if not fms else {
+            "bsr_ms_median": round(pct(fms, .5), 5), "bsr_ms_p90": round(pct(fms, .9), 5),
+            "dense_ms_median": round(pct(fdms, .5), 5),
+            "speedup_vs_dense": round(pct(fdms, .5) / pct(fms, .5), 3),
+            "note": "each launch after a 1 GiB device write (L2 and MALL evicted)"},
         "pack_ms": round(pack_ms, 3),
         "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,

@@ -53,16 +53,21 @@ namespace {
 
 constexpr int NT = 512;             // threads per workgroup: 8 waves
 constexpr int G = GROUP_TILES;      // tile rows per item
-constexpr int NS = 4;               // LDS ring slots
-// Steps go in pairs, one barrier per pair: after the barrier of pair (b, b + 1)
-// each wave loads steps b + 2 and b + 3 into the slots of b - 2 and b - 1.
-constexpr int XU4 = BM * 4;         // 16-byte chunks of one X slice (256 x 32 elements)
-constexpr int WU4 = G * 128;        // 16-byte chunks of G W tiles (32 x 32 elements each)
-constexpr int SLOT = XU4 + WU4;     // one ring slot: 32 KB
+// Steps go in pairs, one barrier per pair.  The LDS ring has two pair slots:
+// after the barrier of pair (b, b + 1) each wave loads steps b + 2 and b + 3
+// into the pair slot that held b - 2 and b - 1.  A pair slot holds the X of
+// both steps interleaved -- row r of the 256 tokens as 128 bytes, the two
+// 64-byte column slices side by side, so that 8 lanes of a DMA instruction
+// fetch a whole 128-byte line when the two columns are adjacent -- and the W
+// tiles of each step (dense W: the group's 256 rows, interleaved like X).
+constexpr int NS = 4;               // steps in flight (two pair slots)
+constexpr int XP_U4 = BM * 8;       // 16-byte chunks of a pair's X (256 x 64 elements): 32 KB
+constexpr int WS_U4 = G * 128;      // 16-byte chunks of one step's W tiles (8 x 32 x 32): 16 KB
+constexpr int PSLOT = XP_U4 + 2 * WS_U4;  // one pair slot: 64 KB
 constexpr int TAB_U4 = 2048;        // per-call tables (walk, slot descriptors, bias): 32 KB
 
-static_assert(XU4 == 2 * 8 * 64 && WU4 == 2 * 8 * 64, "2 X and up to 2 W DMA instructions per wave");
-static_assert((NS * SLOT + TAB_U4) * 16 <= 163840, "LDS budget of one workgroup");
+static_assert(XP_U4 == 8 * 4 * 64 && WS_U4 == 8 * 2 * 64, "4 X and 2 W DMA instructions per wave");
+static_assert((2 * PSLOT + TAB_U4) * 16 <= 163840, "LDS budget of one workgroup");
 
 // A zero line for DMA lanes past K, and a sink for store lanes outside Y.
 static __device__ uint4 g_zero[1];
@@ -145,12 +150,11 @@ __device__ inline void lds_write16(uint32_t addr, v4i v)
     *(__attribute__((address_space(3))) v4i*)(uintptr_t)addr = v;
 }
 
-// X (and dense W) slice layout in LDS: chunk (row r, 16-byte column chunk ch)
-// at r * 4 + (ch ^ swz(r)).  A 16-byte read by 16 lanes (rows r .. r + 15 of
-// one chunk column) then touches 16 different 16-byte bank groups: the LDS
-// serves 256 bytes per clock, and rows 4 apart share a bank group unless the
-// swizzle separates them.
-__device__ inline int xswz(int r) { return ((r >> 1) ^ (r >> 2)) & 3; }
+// Pair X (and dense W) layout in LDS: chunk ch (0..7: 16 bytes; 0..3 the first
+// step's column tile, 4..7 the second's) of row r at r * 8 + (ch ^ swz(r)).
+// A 16-byte read by 16 lanes (rows r .. r + 15 of one chunk) then touches 16
+// different 16-byte bank groups (the LDS serves 256 bytes per clock).
+__device__ inline int xswz(int r) { return (r >> 1) & 7; }
 
 // Walk entry (LDS table): {col | bits << 16 | last step of the item << 24 |
 // last entry of its segment << 25, first tile, start of the next segment in
@@ -173,7 +177,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
 {
     using E = Elem<DT>;
     using F = typename E::frag;
-    __shared__ uint4 smem[NS * SLOT + TAB_U4];
+    __shared__ uint4 smem[2 * PSLOT + TAB_U4];
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
@@ -189,7 +193,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
 
     // ---- per-call tables in LDS: slot descriptors {group, first walk entry,
     // walk length}, walk entries, float32 bias of each slot's 256 outputs
-    char* tab = (char*)(smem + NS * SLOT);
+    char* tab = (char*)(smem + 2 * PSLOT);
     int4* t_desc = (int4*)tab;
     int4* t_walk = (int4*)(tab + a.walk_off);
     float* t_bias = (float*)(tab + a.bias_off);
@@ -215,7 +219,9 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         const int j = i - d.y;  // position in the slot's walk
         int2 e;
         if (DENSE) {
-            int col = (int)((int64_t)(a.gs0 + slot) * ncol / a.n_groups) + j;
+            // the walk starts at an even column: the pair's two columns then
+            // share 128-byte lines of X
+            int col = ((int)((int64_t)(a.gs0 + slot) * ncol / a.n_groups) & ~1) + j;
             if (col >= ncol)
                 col -= ncol;
             e = make_int2(j < ncol ? col | (rows_of(d.x) << 16) : 0, 0);
@@ -244,14 +250,19 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     const uint32_t smem0 = lds_addr(smem);
     const uint32_t walk_lds = lds_addr(t_walk), desc_lds = lds_addr(t_desc), bias_lds = lds_addr(t_bias);
 
-    // Per-lane constants of this wave's DMA instructions.  X / dense W: LDS
-    // chunk p of the slice holds row p / 4, column chunk (p % 4) ^ swz(row).
-    int srow[2], scol[2];
+    // Per-lane constants of this wave's pair DMA (X, dense W): instruction i
+    // fills rows 32 wave + 8 i .. + 7 (1 KB); lane l writes chunk position
+    // l % 8 of row 32 wave + 8 i + l / 8, which holds chunk ch = (l % 8) ^
+    // swz(row): columns (ch % 4) * 8 .. + 7 of the first (ch < 4) or second
+    // step's column tile.
+    int srow[4], scol[4];
+    uint32_t sel2 = 0;  // bit i: instruction i's lane fetches from the second step
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        const int p = (wave * 2 + i) * 64 + lane;
-        srow[i] = p >> 2;
-        scol[i] = ((p & 3) ^ xswz(p >> 2)) * 8;
+    for (int i = 0; i < 4; ++i) {
+        srow[i] = wave * 32 + i * 8 + (lane >> 3);
+        const int ch = (lane & 7) ^ xswz(srow[i]);
+        scol[i] = (ch & 3) * 8;
+        sel2 |= (uint32_t)(ch >> 2) << i;
     }
 
     // ---- producer: item pk (slot p_slot of token tile p_mt), segment
@@ -259,31 +270,27 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     int pk = 0;
     int p_mt = item_off / a.n_slots;
     int p_slot = item_off - p_mt * a.n_slots;
-    // X of the producer's item: a uniform base (first row of the token tile;
-    // the second instruction's base is 1 KB lower, see dma16i) and per-lane
-    // byte offsets of row min(row, M - 1 - m0), column chunk.  Dense W: the
-    // same for the item's group of output rows (rows past N repeat its last).
+    // X of the producer's item: a uniform base (first row of the token tile)
+    // and per-lane byte offsets of row min(row, M - 1 - m0), column chunk.
+    // Dense W: the same for the item's group of output rows (rows past N
+    // repeat its last).  Instruction i uses the base minus i KB (see dma16i).
     const char* xbase;
-    const char* xbase_k;
-    uint32_t xoff[2];
+    uint32_t xoff[4];
     const char* wibase = nullptr;
-    const char* wibase_k = nullptr;
-    uint32_t wioff[2] = {0, 0};
+    uint32_t wioff[4] = {0, 0, 0, 0};
     auto set_x = [&]() {
         const int64_t m0 = (int64_t)p_mt * BM;
         xbase = X + m0 * a.ldx * 2;
-        xbase_k = xbase - 1024;
         const int last_row = (int)min((int64_t)BM - 1, a.M - 1 - m0);
 #pragma unroll
-        for (int i = 0; i < 2; ++i)
+        for (int i = 0; i < 4; ++i)
             xoff[i] = (uint32_t)((min(srow[i], last_row) * a.ldx + scol[i]) * 2);
         if (DENSE) {
             const int64_t n0 = (int64_t)t_desc[p_slot].x * G * TILE;
             wibase = W + n0 * a.ldw * 2;
-            wibase_k = wibase - 1024;
             const int wlast = (int)min((int64_t)G * TILE - 1, a.N - 1 - n0);
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int i = 0; i < 4; ++i)
                 wioff[i] = (uint32_t)((min(srow[i], wlast) * a.ldw + scol[i]) * 2);
         }
     };
@@ -296,8 +303,10 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     v4i cur = *(const v4i*)&t_walk[min(t_desc[p_slot].y + lane, a.n_walk - 1)];
     v4i nxt = *(const v4i*)&t_walk[min(__builtin_amdgcn_readlane(cur.z, 0) + lane, a.n_walk - 1)];
 
-    // One step's DMA for this wave: the ring slot, the instruction count (2 or
-    // 4), the column tile and its byte offset in a row of X / dense W, and
+    // One step's DMA for this wave: the step's ring position (step & 3: pair
+    // slot (step >> 1) & 1, half step & 1), whether it loads anything (n: 0
+    // for a step that keeps no tile, 2 with X only, 4 with this wave's W
+    // tile), the column tile and its byte offset in a row of X / dense W, and
     // (sparse) the byte offset of this wave's W tile in the tile stream.
     struct Dma {
         int slot, n, col;
@@ -353,71 +362,106 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         }
         return e;
     };
-    // Instruction j (0, 1: X; 2, 3: W) of a prepared step, in the general form
-    // (last column tile of a K that is not a multiple of 32: lanes past K read
-    // the zero line).
-    auto dma_issue_tail = [&](const Dma d, int j) {
-        uint4* dst = smem + d.slot * SLOT + (j < 2 ? 0 : XU4) + wave * 128 + (j & 1) * 64;
-        const int i = j & 1;
-        if (j < 2 || DENSE) {
-            if (d.col * TILE + scol[i] >= a.K)
-                dma16(zero, dst);
-            else if (j < 2)
-                dma16(xbase, xoff[i] + d.xcol, dst);
-            else
-                dma16(wibase, wioff[i] + d.xcol, dst);
-        } else {
-            dma16(stream, loff + d.woff + i * 1024, dst);
-        }
-    };
-
-    // All instructions of a prepared step: its X, then its W if any.  X and W
-    // each take one M0 value for their two instructions.
-    auto dma_all = [&](const Dma d) {
-        if (d.n < 2)
+    // The DMA of a pair of prepared steps (d0, d1) into their pair slot, in
+    // two parts.  X: 4 instructions of one M0 value (none if neither step
+    // keeps a tile); lanes past K read the zero line.  W: dense, the group's
+    // 256 rows of both column tiles (4 instructions, laid out like X); sparse,
+    // this wave's tile of each step that keeps it (2 instructions each).
+    auto dma_x = [&](const Dma d0, const Dma d1) {
+        if (d0.n == 0 && d1.n == 0)
             return;
-        if (KTAIL && d.col == ncol - 1) {
+        const int ps = (d0.slot >> 1) & 1;
+        if (KTAIL && (d0.col == ncol - 1 || d1.col == ncol - 1)) {
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (j < d.n)
-                    dma_issue_tail(d, j);
+            for (int i = 0; i < 4; ++i) {
+                const bool second = (sel2 >> i) & 1;
+                const int col = second ? d1.col : d0.col;
+                uint4* dx = smem + ps * PSLOT + wave * 256 + i * 64;
+                if (col * TILE + scol[i] >= a.K)
+                    dma16(zero, dx);
+                else
+                    dma16(xbase, xoff[i] + (second ? d1.xcol : d0.xcol), dx);
+            }
             return;
         }
-        const uint32_t mx = smem0 + (uint32_t)(d.slot * SLOT + wave * 128) * 16;
-        dma16i<0>(xbase, xoff[0] + d.xcol, mx);
-        dma16i<1024>(xbase_k, xoff[1] + d.xcol, mx);
-        if (d.n == 4) {
-            const uint32_t mw = mx + XU4 * 16;
-            if (DENSE) {
-                dma16i<0>(wibase, wioff[0] + d.xcol, mw);
-                dma16i<1024>(wibase_k, wioff[1] + d.xcol, mw);
-            } else {
-                dma16i<0>(stream, loff + d.woff, mw);
-                dma16i<1024>(stream, loff + d.woff, mw);
+        const uint32_t mx = smem0 + (uint32_t)ps * (PSLOT * 16) + (uint32_t)wave * 4096;
+        uint32_t vo[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+            vo[i] = ((sel2 >> i) & 1) ? d1.xcol : d0.xcol;
+        dma16i<0>(xbase, xoff[0] + vo[0], mx);
+        dma16i<1024>(xbase - 1024, xoff[1] + vo[1], mx);
+        dma16i<2048>(xbase - 2048, xoff[2] + vo[2], mx);
+        dma16i<3072>(xbase - 3072, xoff[3] + vo[3], mx);
+    };
+    auto dma_w = [&](const Dma d0, const Dma d1) {
+        const int ps = (d0.slot >> 1) & 1;
+        const uint32_t wa = smem0 + (uint32_t)(ps * PSLOT + XP_U4) * 16;
+        if (DENSE) {
+            if (d0.n == 0 && d1.n == 0)
+                return;
+            if (KTAIL && (d0.col == ncol - 1 || d1.col == ncol - 1)) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const bool second = (sel2 >> i) & 1;
+                    const int col = second ? d1.col : d0.col;
+                    uint4* dw = smem + ps * PSLOT + XP_U4 + wave * 256 + i * 64;
+                    if (col * TILE + scol[i] >= a.K)
+                        dma16(zero, dw);
+                    else
+                        dma16(wibase, wioff[i] + (second ? d1.xcol : d0.xcol), dw);
+                }
+                return;
+            }
+            const uint32_t mw = wa + (uint32_t)wave * 4096;
+            uint32_t vo[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+                vo[i] = ((sel2 >> i) & 1) ? d1.xcol : d0.xcol;
+            dma16i<0>(wibase, wioff[0] + vo[0], mw);
+            dma16i<1024>(wibase - 1024, wioff[1] + vo[1], mw);
+            dma16i<2048>(wibase - 2048, wioff[2] + vo[2], mw);
+            dma16i<3072>(wibase - 3072, wioff[3] + vo[3], mw);
+        } else {
+            if (d0.n == 4) {
+                const uint32_t mw = wa + (uint32_t)wave * 2048;
+                dma16i<0>(stream, loff + d0.woff, mw);
+                dma16i<1024>(stream, loff + d0.woff, mw);
+            }
+            if (d1.n == 4) {
+                const uint32_t mw = wa + WS_U4 * 16 + (uint32_t)wave * 2048;
+                dma16i<0>(stream, loff + d1.woff, mw);
+                dma16i<1024>(stream, loff + d1.woff, mw);
             }
         }
     };
 
     // ---- prologue: the first pair of steps
     uint64_t q = 0;  // queue entries of steps t, t + 1, ... (E_BITS each)
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        Dma d;
-        q |= (uint64_t)(uint32_t)p_prepare(i, d) << (E_BITS * i);
-        dma_all(d);
+    {
+        Dma d0, d1;
+        q |= (uint64_t)(uint32_t)p_prepare(0, d0);
+        q |= (uint64_t)(uint32_t)p_prepare(1, d1) << E_BITS;
+        dma_x(d0, d1);
+        dma_w(d0, d1);
     }
 
-    // LDS read addresses of this lane (slot 0; token half u = 1 is +2048 bytes)
-    uint32_t xa_addr[2], wd_addr[2];
+    // LDS read addresses of this lane in pair slot 0, by (half of the pair s,
+    // k-step ks); token half u = 1 is +4096 bytes (32 rows), dense tile row
+    // 4h + j is +4096 j bytes (xswz(r + 32) = xswz(r))
+    uint32_t xa_addr[2][2], wd_addr[2][2];
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-        const int r = wm * 64 + (lane & 31);
-        const int ch = ks * 2 + (lane >> 5);
-        xa_addr[ks] = smem0 + (r * 4 + (ch ^ xswz(r))) * 16;
-        const int rw = wh * 128 + (lane & 31);  // dense: tile row 4h + j is +j * 2048
-        wd_addr[ks] = smem0 + XU4 * 16 + (rw * 4 + (ch ^ xswz(rw))) * 16;
+    for (int sh = 0; sh < 2; ++sh) {
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            const int ch = sh * 4 + ks * 2 + (lane >> 5);
+            const int r = wm * 64 + (lane & 31);
+            xa_addr[sh][ks] = smem0 + (r * 8 + (ch ^ xswz(r))) * 16;
+            const int rw = wh * 128 + (lane & 31);
+            wd_addr[sh][ks] = smem0 + XP_U4 * 16 + (rw * 8 + (ch ^ xswz(rw))) * 16;
+        }
     }
-    const uint32_t wa_addr = smem0 + XU4 * 16 + wh * 4 * 2048 + lane * 16;  // this half's rows
+    const uint32_t wa_addr = smem0 + XP_U4 * 16 + wh * 4 * 2048 + lane * 16;  // this half's rows
 
     // Operands of one half step (one 16-column k-step of a column tile): this
     // wave's two X fragments (token halves) and its kept W fragments.
@@ -426,20 +470,21 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     };
     // LDS reads of half step (t, ks)
     auto read_half = [&](Ops& o, int t, int ks) {
-        const uint32_t slot_off = (uint32_t)(t & (NS - 1)) * (SLOT * 16);
-        o.x[0] = lds_read16<0>(xa_addr[ks] + slot_off);
-        o.x[1] = lds_read16<2048>(xa_addr[ks] + slot_off);
+        const int sh = t & 1;
+        const uint32_t ps_off = (uint32_t)((t >> 1) & 1) * (PSLOT * 16);
+        o.x[0] = lds_read16<0>(xa_addr[sh][ks] + ps_off);
+        o.x[1] = lds_read16<4096>(xa_addr[sh][ks] + ps_off);
         // four W fragments whatever the mask (no branch): rows 4h .. 4h + 3
         // of the group, at fixed offsets in both layouts
         if (DENSE) {
-            o.w[0] = lds_read16<0 * 2048>(wd_addr[ks] + slot_off);
-            o.w[1] = lds_read16<1 * 2048>(wd_addr[ks] + slot_off);
-            o.w[2] = lds_read16<2 * 2048>(wd_addr[ks] + slot_off);
-            o.w[3] = lds_read16<3 * 2048>(wd_addr[ks] + slot_off);
+            o.w[0] = lds_read16<0 * 4096>(wd_addr[sh][ks] + ps_off);
+            o.w[1] = lds_read16<1 * 4096>(wd_addr[sh][ks] + ps_off);
+            o.w[2] = lds_read16<2 * 4096>(wd_addr[sh][ks] + ps_off);
+            o.w[3] = lds_read16<3 * 4096>(wd_addr[sh][ks] + ps_off);
         } else {
-            // row j of the group's tile lies at W position j (a dropped row's
-            // position holds stale data and is never used)
-            const uint32_t wa = wa_addr + slot_off + ks * 1024;
+            // row j of the group's tile lies at W position j of the step's W
+            // area (a dropped row's position holds stale data and is never used)
+            const uint32_t wa = wa_addr + ps_off + (uint32_t)sh * (WS_U4 * 16) + ks * 1024;
             o.w[0] = lds_read16<0 * 2048>(wa);
             o.w[1] = lds_read16<1 * 2048>(wa);
             o.w[2] = lds_read16<2 * 2048>(wa);
@@ -562,11 +607,13 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     auto flush = [&](int sslot) {
         const int64_t mw = f_mw, nw = f_nw;
         const bool inside = f_inside;
-        // staging: token tau (0..31) of a round at region tau / 16 (X part,
-        // then W part of this wave's DMA area), row tau % 16 of 128 bytes,
-        // 16-byte chunk k at k ^ ((tau / 2) % 8): conflict-free both ways
-        const uint32_t st0 = smem0 + (uint32_t)(sslot * SLOT + wave * 128) * 16;
-        const uint32_t st1 = st0 + XU4 * 16;
+        // staging: token tau (0..31) of a round at region tau / 16 of this
+        // wave's own W area of the pair slot (the part its next W DMA refills),
+        // row tau % 16 of 128 bytes, 16-byte chunk k at k ^ ((tau / 2) % 8):
+        // conflict-free both ways
+        const uint32_t st0 = smem0 + (uint32_t)(sslot * PSLOT + XP_U4) * 16 +
+                             (uint32_t)wave * (DENSE ? 4096 : 2048);
+        const uint32_t st1 = st0 + (DENSE ? 2048 : WS_U4 * 16);
         const int b = lane & 31;
         const uint32_t wbase = (b < 16 ? st0 : st1) + (b & 15) * 128;
         const int wswz = (b >> 1) & 7;
@@ -610,28 +657,28 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
 
     // Barrier of pair (b, b + 1): every wave has waited for all of its DMA
     // (steps b and b + 1, and its stores) and finished with steps b - 2 and
-    // b - 1; their slots are free afterwards.
+    // b - 1; their pair slot is free afterwards.
     auto sync = [&]() { asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory"); };
     int t = 0;
-    // prepare and issue the DMA of step t + ahead (steps are prepared in order)
-    auto load = [&](int ahead) {
-        Dma d;
-        q |= (uint64_t)(uint32_t)p_prepare((t + ahead) & (NS - 1), d) << (ahead * E_BITS);
-        dma_all(d);
-    };
     sync();  // the first pair has landed
     // One item per iteration (items have an even number of steps).  After its
-    // last pair: pack(), the next barrier (which frees the slots of that
-    // pair), the stores through the slot of the last step (flush), then the
-    // DMA into that slot and the next item's accumulators.  The packed
-    // outputs and the accumulators are never live together.
+    // last pair: pack(), the next barrier (which frees that pair's slot), the
+    // X DMA of steps t + 2 and t + 3, the stores staged through this wave's W
+    // area of the free pair slot (flush), then their W DMA and the next item's
+    // accumulators.  The packed outputs and the accumulators are never live
+    // together.
     bool have = false;  // pko holds an item not yet stored
     for (;;) {
         read_half(r0, t, 0);
-        load(2);  // into the slot of step t - 2
-        if (have)
-            flush((t - 1) & (NS - 1));
-        load(3);  // into the slot of step t - 1, after the stores left it
+        {
+            Dma d0, d1;
+            q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
+            q |= (uint64_t)(uint32_t)p_prepare((t + 3) & (NS - 1), d1) << (3 * E_BITS);
+            dma_x(d0, d1);
+            if (have)
+                flush(((t + 2) >> 1) & 1);
+            dma_w(d0, d1);
+        }
         init_acc(c_slot);
         for (;;) {  // the pairs of the item
             const int e0 = (int)(q & E_MASK), e1 = (int)((q >> E_BITS) & E_MASK);
@@ -645,8 +692,11 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             if (e1 & E_LAST)
                 break;
             read_half(r0, t, 0);
-            load(2);
-            load(3);
+            Dma d0, d1;
+            q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
+            q |= (uint64_t)(uint32_t)p_prepare((t + 3) & (NS - 1), d1) << (3 * E_BITS);
+            dma_x(d0, d1);
+            dma_w(d0, d1);
         }
         pack();
         have = true;
@@ -659,7 +709,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             ++c_mt;
         }
     }
-    flush((t - 1) & (NS - 1));
+    flush(((t - 1) >> 1) & 1);
     // no DMA or store of this workgroup may be in flight when it ends
     __builtin_amdgcn_s_waitcnt(0);
 }

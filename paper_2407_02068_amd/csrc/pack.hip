@@ -155,11 +155,12 @@ __global__ __launch_bounds__(PLAN_THREADS) void k_pack_plan(PackArgs a, int32_t*
     for (int g = tid; g < a.n_groups; g += PLAN_THREADS) {
         const int rank = s_rank[g];
         const int ns = (g + 1 < a.n_groups ? s_gsteps[g + 1] : n_steps) - s_gsteps[g];
-        // the walk of slot `rank` starts at column step rank * ns / n_groups and
-        // wraps: slots that run side by side on one token tile read different X
-        // columns at a time
+        // the walk of slot `rank` starts at column step rank * ns / n_groups,
+        // rounded down to even (the kernel's pairs then tend to cover aligned
+        // column pairs), and wraps: slots that run side by side on one token
+        // tile read different X columns at a time
         gdesc[rank] = make_int4(g, s_walk[rank], (max(ns, 1) + 1) & ~1,
-                                ns > 0 ? (int)((int64_t)rank * ns / a.n_groups) : 0);
+                                ns > 0 ? (int)((int64_t)rank * ns / a.n_groups) & ~1 : 0);
     }
     if (tid == 0) {
         row_ptr[a.R] = nnzb;
