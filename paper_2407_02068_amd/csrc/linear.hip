@@ -78,7 +78,10 @@ struct Dims {
     int32_t n_tile_rows, n_tile_cols, n_groups;
     int32_t gs0, n_slots;   // this launch: launch slots [gs0, gs0 + n_slots) ...
     int32_t n_items;        // ... times every token tile
-    int32_t p_div, p_mod;   // grid size divided by / modulo n_slots
+    int32_t xcd_tiles;      // item order: 1 = each XCD owns whole token tiles
+    int32_t p_div, p_mod;   // from one item of a workgroup to its next: token
+                            // tiles and launch slots to advance, ...
+    int32_t mt_carry;       // ... and token tiles more when the slot wraps
     int32_t walk0, n_walk;  // this launch's slice of the walk array
     int32_t walk_off, bias_off;  // byte offsets of the walk and bias tables in LDS
 };
@@ -183,11 +186,27 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
     const int wm = wave & 3, wh = wave >> 2;
 
-    // this workgroup's items: k * P + item_off, k = 0, 1, ...; the 32 compute
-    // units of one XCD (blockIdx % 8) take 32 consecutive items
-    const int P = (int)gridDim.x;
-    const int item_off = (int)(blockIdx.x & 7) * (P >> 3) + (int)(blockIdx.x >> 3);
-    const int my_items = item_off < a.n_items ? (a.n_items - item_off + P - 1) / P : 0;
+    // This workgroup's items.  Items are (token tile, launch slot) pairs,
+    // slot-minor; workgroup b runs on XCD x = b % 8 as its c = b / 8-th of
+    // C = P / 8.  xcd_tiles: XCD x owns token tiles x, x + 8, ... with all their
+    // slots and deals them to its C workgroups in turn (c, c + C, ...), so
+    // the items of one token tile share that XCD's L2.  Otherwise item
+    // x C + c + k P, k = 0, 1, ...: an XCD's workgroups take C consecutive items.
+    const int P = (int)gridDim.x, C = P >> 3;
+    const int xcd = (int)(blockIdx.x & 7), cu = (int)(blockIdx.x >> 3);
+    int first_mt, first_slot, my_items;
+    if (a.xcd_tiles) {
+        const int n_mt = a.n_items / a.n_slots;
+        const int n_local = xcd < n_mt ? (n_mt - xcd + 7) / 8 * a.n_slots : 0;
+        my_items = cu < n_local ? (n_local - cu + C - 1) / C : 0;
+        first_mt = xcd + 8 * (cu / a.n_slots);
+        first_slot = cu % a.n_slots;
+    } else {
+        const int item_off = xcd * C + cu;
+        my_items = item_off < a.n_items ? (a.n_items - item_off + P - 1) / P : 0;
+        first_mt = item_off / a.n_slots;
+        first_slot = item_off % a.n_slots;
+    }
     if (my_items == 0)
         return;
 
@@ -268,8 +287,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // ---- producer: item pk (slot p_slot of token tile p_mt), segment
     // entries in lanes (cur) and the next segment (nxt), position p_i
     int pk = 0;
-    int p_mt = item_off / a.n_slots;
-    int p_slot = item_off - p_mt * a.n_slots;
+    int p_mt = first_mt;
+    int p_slot = first_slot;
     // X of the producer's item: a uniform base (first row of the token tile)
     // and per-lane byte offsets of row min(row, M - 1 - m0), column chunk.
     // Dense W: the same for the item's group of output rows (rows past N
@@ -356,7 +375,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             p_mt += a.p_div;
             if (p_slot >= a.n_slots) {
                 p_slot -= a.n_slots;
-                ++p_mt;
+                p_mt += a.mt_carry;
             }
             x_stale = true;
         }
@@ -494,8 +513,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
 
     // consumer cursor
     int ck = 0;
-    int c_mt = item_off / a.n_slots;
-    int c_slot = item_off - c_mt * a.n_slots;
+    int c_mt = first_mt;
+    int c_slot = first_slot;
 
     // Accumulators start at the bias of their outputs: lane l, register 4 qq
     // + i of tile row j holds output 8 qq + 4 (l / 32) + i of that row.
@@ -706,7 +725,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         c_mt += a.p_div;
         if (c_slot >= a.n_slots) {
             c_slot -= a.n_slots;
-            ++c_mt;
+            c_mt += a.mt_carry;
         }
     }
     flush(((t - 1) >> 1) & 1);
@@ -822,8 +841,22 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
         const int need = (d.n_items + 7) / 8 * 8;
         if (P > need)
             P = need;
-        d.p_div = P / ns;
-        d.p_mod = P % ns;
+        // Each XCD owns whole token tiles (its L2 then holds a tile's X for
+        // all the tile's items) unless that deals some workgroup more items
+        // than the plain order does.
+        const int C = P / 8;
+        const int64_t plain_max = (items + P - 1) / P;
+        const int64_t xcd_max = ((n_mt + 7) / 8 * ns + C - 1) / C;
+        d.xcd_tiles = n_mt >= 8 && xcd_max <= plain_max;
+        if (d.xcd_tiles) {
+            d.p_div = 8 * (C / ns);
+            d.p_mod = C % ns;
+            d.mt_carry = 8;
+        } else {
+            d.p_div = P / ns;
+            d.p_mod = P % ns;
+            d.mt_carry = 1;
+        }
         const dim3 grid(P), block(NT);
 #define LPV_LAUNCH1(DT_, GELU_, KT_)                                                              \
     hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_>), grid, block, 0, s, d, a.X, a.stream, \
