@@ -52,6 +52,13 @@ class Oracle:
         lib.lpvo_keep_count.restype = i64
         lib.lpvo_mask_topk.argtypes = [vp, i64, i64, vp]
         lib.lpvo_mask_topk.restype = i32
+        lib.lpvo_grad_x.argtypes = [i32, vp, i64, i64, vp, i64, i64, i64, i32, i32, vp, vp,
+                                    i64, i32]
+        lib.lpvo_grad_x.restype = i32
+        lib.lpvo_grad_w.argtypes = [i32, vp, i64, vp, i64, i64, i64, i64, i32, i32, vp, vp]
+        lib.lpvo_grad_w.restype = i64
+        lib.lpvo_grad_bias.argtypes = [i32, vp, i64, i64, i64, vp]
+        lib.lpvo_grad_bias.restype = i32
         self.lib = lib
         self.path = path
 
@@ -135,6 +142,64 @@ class Oracle:
             raise RuntimeError("lpvo_linear failed (%d)" % rc)
         return Y
 
+
+    def _grid(self, N, K, b_r, b_c, mask):
+        if b_r <= 0 or b_c <= 0 or N % b_r or K % b_c:
+            raise ValueError("block %dx%d does not divide weight %dx%d" % (b_r, b_c, N, K))
+        mask = np.ascontiguousarray(mask, dtype=np.uint8)
+        if mask.shape != (N // b_r, K // b_c):
+            raise ValueError("mask shape %s, expected %s" % (mask.shape, (N // b_r, K // b_c)))
+        return mask
+
+    def grad_x(self, G, W, dtype, b_r, b_c, mask, nthreads=None):
+        """``dX = G W~`` in float64 (M x K): the input gradient for the
+        pre-activation gradient ``G`` (M x N)."""
+        G = np.ascontiguousarray(G)
+        W = np.ascontiguousarray(W)
+        _check(G, dtype, "G")
+        _check(W, dtype, "W")
+        M, N = G.shape
+        N2, K = W.shape
+        if N2 != N:
+            raise ValueError("G is %dx%d but W is %dx%d" % (M, N, N2, K))
+        mask = self._grid(N, K, b_r, b_c, mask)
+        dX = np.empty((M, K), np.float64)
+        nt = default_threads() if nthreads is None else int(nthreads)
+        rc = self.lib.lpvo_grad_x(_CODES[dtype], _ptr(G), N, M, _ptr(W), K, N, K, b_r, b_c,
+                                  _ptr(mask), _ptr(dX), K, nt)
+        if rc:
+            raise RuntimeError("lpvo_grad_x failed (%d)" % rc)
+        return dX
+
+    def grad_w(self, G, X, dtype, b_r, b_c, mask):
+        """``G^T X`` on the kept blocks only, float64 ``[nnzb, b_r, b_c]`` in BSR
+        order (the order of :meth:`pack`'s values)."""
+        G = np.ascontiguousarray(G)
+        X = np.ascontiguousarray(X)
+        _check(G, dtype, "G")
+        _check(X, dtype, "X")
+        M, N = G.shape
+        M2, K = X.shape
+        if M2 != M:
+            raise ValueError("G is %dx%d but X is %dx%d" % (M, N, M2, K))
+        mask = self._grid(N, K, b_r, b_c, mask)
+        nnzb = int(mask.astype(bool).sum())
+        out = np.empty((nnzb, b_r, b_c), np.float64)
+        got = self.lib.lpvo_grad_w(_CODES[dtype], _ptr(G), N, _ptr(X), K, M, N, K, b_r, b_c,
+                                   _ptr(mask), _ptr(out))
+        if got != nnzb:
+            raise RuntimeError("lpvo_grad_w returned %d, expected %d blocks" % (got, nnzb))
+        return out
+
+    def grad_bias(self, G, dtype):
+        """``db[n] = sum_m G[m][n]`` in float64."""
+        G = np.ascontiguousarray(G)
+        _check(G, dtype, "G")
+        M, N = G.shape
+        db = np.empty(N, np.float64)
+        if self.lib.lpvo_grad_bias(_CODES[dtype], _ptr(G), N, M, N, _ptr(db)):
+            raise ValueError("lpvo_grad_bias rejected its arguments")
+        return db
 
     def block_scores(self, W, dtype, b_r, b_c, G=None):
         """Block scores, float64 R x C: the mean of |W * G| per block (the
@@ -231,6 +296,18 @@ def unpack(row_ptr, col_idx, values, dtype, N, K, b_r, b_c):
 
 def linear(X, W, dtype, b_r, b_c, mask, bias=None, gelu=False, nthreads=None):
     return default().linear(X, W, dtype, b_r, b_c, mask, bias, gelu, nthreads)
+
+
+def grad_x(G, W, dtype, b_r, b_c, mask, nthreads=None):
+    return default().grad_x(G, W, dtype, b_r, b_c, mask, nthreads)
+
+
+def grad_w(G, X, dtype, b_r, b_c, mask):
+    return default().grad_w(G, X, dtype, b_r, b_c, mask)
+
+
+def grad_bias(G, dtype):
+    return default().grad_bias(G, dtype)
 
 
 def block_scores(W, dtype, b_r, b_c, G=None):

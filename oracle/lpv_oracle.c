@@ -402,3 +402,154 @@ int lpvo_mask_topk(const double* scores, int64_t n_blocks, int64_t n_keep, uint8
     free(order);
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* Backward of the block-sparse linear layer (finetuning, Sec. 3.1 / Fig. 1)  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * After pruning, the paper finetunes the pruned model.  The block mask stays
+ * fixed while finetuning: a dropped block is absent from the layer, so it
+ * neither passes a gradient to the input nor receives one.  For the
+ * pre-activation Z = X W~^T + b and its gradient G = dL/dZ (M x N; with the
+ * GELU epilogue the caller first multiplies dL/dY by g'(Z) element-wise), the
+ * chain rule gives, in float64:
+ *   dX[m][k] = sum_{n=0}^{N-1} G[m][n] * W~[n][k]       (n ascending)
+ *   dW[n][k] = sum_{m=0}^{M-1} G[m][n] * X[m][k]        (m ascending), only for
+ *              (n, k) in a kept block, returned block by block in the BSR order
+ *              of lpvo_pack (block-rows ascending, kept columns ascending, each
+ *              block b_r rows of b_c values)
+ *   db[n]    = sum_{m=0}^{M-1} G[m][n]                  (m ascending)
+ */
+
+struct gradx_job {
+    int dtype;
+    const void* G;
+    int64_t ldg;
+    int64_t m_begin, m_end;
+    const double* Wd; /* [N][K]: the expanded, pruned weight */
+    int64_t N, K;
+    double* dX;
+    int64_t lddx;
+};
+
+static void* gradx_rows(void* arg)
+{
+    struct gradx_job* j = (struct gradx_job*)arg;
+    for (int64_t m = j->m_begin; m < j->m_end; ++m) {
+        double* out = j->dX + m * j->lddx;
+        for (int64_t k = 0; k < j->K; ++k)
+            out[k] = 0.0;
+        /* out[k] = sum over n ascending of G[m][n] * W~[n][k] */
+        for (int64_t n = 0; n < j->N; ++n) {
+            const double g = dec_one(j->dtype, j->G, m * j->ldg + n);
+            const double* wn = j->Wd + n * j->K;
+            for (int64_t k = 0; k < j->K; ++k)
+                out[k] += g * wn[k];
+        }
+    }
+    return NULL;
+}
+
+int lpvo_grad_x(int dtype, const void* G, int64_t ldg, int64_t M, const void* W, int64_t ldw,
+                int64_t N, int64_t K, int b_r, int b_c, const uint8_t* mask, double* dX,
+                int64_t lddx, int nthreads)
+{
+    if (!lpvo_elem_size(dtype) || !grid_ok(N, K, b_r, b_c) || M < 0 || ldg < N || ldw < K ||
+        lddx < K || !mask || (M > 0 && (!G || !dX)) || (N * K > 0 && !W))
+        return -1;
+    if (M == 0 || K == 0)
+        return 0;
+    const int64_t C = K / b_c;
+    double* Wd = (double*)malloc(sizeof(double) * (size_t)(N * K + 1));
+    if (!Wd)
+        return -2;
+    for (int64_t n = 0; n < N; ++n)
+        for (int64_t k = 0; k < K; ++k)
+            Wd[n * K + k] = mask[(n / b_r) * C + (k / b_c)] ? dec_one(dtype, W, n * ldw + k) : 0.0;
+    if (nthreads < 1)
+        nthreads = 1;
+    if (nthreads > M)
+        nthreads = (int)M;
+    struct gradx_job* jobs = (struct gradx_job*)calloc((size_t)nthreads, sizeof *jobs);
+    pthread_t* tid = (pthread_t*)calloc((size_t)nthreads, sizeof *tid);
+    char* running = (char*)calloc((size_t)nthreads, 1);
+    int rc = 0;
+    if (!jobs || !tid || !running) {
+        rc = -2;
+        goto out;
+    }
+    for (int t = 0; t < nthreads; ++t)
+        jobs[t] = (struct gradx_job){dtype, G, ldg, M * t / nthreads, M * (t + 1) / nthreads,
+                                     Wd, N, K, dX, lddx};
+    for (int t = 1; t < nthreads; ++t)
+        running[t] = pthread_create(&tid[t], NULL, gradx_rows, &jobs[t]) == 0;
+    for (int t = 0; t < nthreads; ++t)
+        if (!running[t])
+            gradx_rows(&jobs[t]);
+    for (int t = 1; t < nthreads; ++t)
+        if (running[t])
+            pthread_join(tid[t], NULL);
+out:
+    free(jobs);
+    free(tid);
+    free(running);
+    free(Wd);
+    return rc;
+}
+
+int64_t lpvo_grad_w(int dtype, const void* G, int64_t ldg, const void* X, int64_t ldx, int64_t M,
+                    int64_t N, int64_t K, int b_r, int b_c, const uint8_t* mask, double* dW)
+{
+    if (!lpvo_elem_size(dtype) || !grid_ok(N, K, b_r, b_c) || M < 0 || ldg < N || ldx < K ||
+        !mask || (M > 0 && (!G || !X)))
+        return -1;
+    const int64_t R = N / b_r, C = K / b_c;
+    int64_t p = 0; /* kept blocks so far, in BSR order */
+    double* g = (double*)malloc(sizeof(double) * (size_t)(b_r > 0 ? b_r : 1));
+    double* x = (double*)malloc(sizeof(double) * (size_t)(b_c > 0 ? b_c : 1));
+    if (!g || !x) {
+        free(g);
+        free(x);
+        return -2;
+    }
+    for (int64_t r = 0; r < R; ++r) {
+        for (int64_t c = 0; c < C; ++c) {
+            if (!mask[r * C + c])
+                continue;
+            if (dW) {
+                double* out = dW + p * b_r * b_c;
+                for (int64_t e = 0; e < (int64_t)b_r * b_c; ++e)
+                    out[e] = 0.0;
+                /* every element: sum over m ascending of G[m][n] * X[m][k] */
+                for (int64_t m = 0; m < M; ++m) {
+                    for (int i = 0; i < b_r; ++i)
+                        g[i] = dec_one(dtype, G, m * ldg + r * b_r + i);
+                    for (int j = 0; j < b_c; ++j)
+                        x[j] = dec_one(dtype, X, m * ldx + c * b_c + j);
+                    for (int i = 0; i < b_r; ++i)
+                        for (int j = 0; j < b_c; ++j)
+                            out[i * b_c + j] += g[i] * x[j];
+                }
+            }
+            ++p;
+        }
+    }
+    free(g);
+    free(x);
+    return p;
+}
+
+int lpvo_grad_bias(int dtype, const void* G, int64_t ldg, int64_t M, int64_t N, double* db)
+{
+    if (!lpvo_elem_size(dtype) || M < 0 || N < 0 || ldg < N || (N > 0 && !db) ||
+        (M > 0 && N > 0 && !G))
+        return -1;
+    for (int64_t n = 0; n < N; ++n) {
+        double s = 0.0;
+        for (int64_t m = 0; m < M; ++m)
+            s += dec_one(dtype, G, m * ldg + n);
+        db[n] = s;
+    }
+    return 0;
+}

@@ -62,6 +62,22 @@ int64_t lpvo_keep_count(int64_t n_blocks, int sparsity_pct);
  * -1 on a bad argument (NaN scores included), -2 when host memory runs out. */
 int lpvo_mask_topk(const double* scores, int64_t n_blocks, int64_t n_keep, uint8_t* mask);
 
+/* Backward of the layer for G = dL/dZ at the pre-activation Z = X W~^T + b
+ * (M x N, row stride ldg), in float64, the mask held fixed:
+ *   lpvo_grad_x: dX (M x K, row stride lddx) = G W~, summed over n ascending;
+ *     rows split over nthreads host threads.  Returns 0, -1 on a bad argument,
+ *     -2 when host memory runs out.
+ *   lpvo_grad_w: dW restricted to the kept blocks, G^T X summed over m
+ *     ascending, written block by block in lpvo_pack's order (nnzb x b_r x b_c;
+ *     dW may be NULL to count).  Returns the kept-block count, -1 or -2.
+ *   lpvo_grad_bias: db[n] = sum over m ascending of G[m][n].  Returns 0 or -1. */
+int lpvo_grad_x(int dtype, const void* G, int64_t ldg, int64_t M, const void* W, int64_t ldw,
+                int64_t N, int64_t K, int b_r, int b_c, const uint8_t* mask, double* dX,
+                int64_t lddx, int nthreads);
+int64_t lpvo_grad_w(int dtype, const void* G, int64_t ldg, const void* X, int64_t ldx, int64_t M,
+                    int64_t N, int64_t K, int b_r, int b_c, const uint8_t* mask, double* dW);
+int lpvo_grad_bias(int dtype, const void* G, int64_t ldg, int64_t M, int64_t N, double* db);
+
 #ifdef __cplusplus
 }
 #endif

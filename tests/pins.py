@@ -10,7 +10,9 @@ Independent references used here: the hand-worked fixture under ``golden/``,
 the standard normal table, ``scipy.sparse.bsr_matrix`` (BSR arrays),
 ``numpy.matmul`` / ``numpy.kron`` (dense products, mask expansion), integer
 arithmetic in int64, torch's CPU bf16 conversion and numpy's float16, and
-numpy's reshape-sum and lexsort (block scores, the top-k order).
+numpy's reshape-sum and lexsort (block scores, the top-k order); for the
+backward, the forward oracle itself (each gradient is checked as the adjoint of
+the pinned forward map) besides numpy products and int64 sums.
 """
 import json
 import math
@@ -399,6 +401,97 @@ def pin_topk_ties_to_lower_index(orc):
     assert np.array_equal(orc.mask_topk(d, 5).reshape(-1), (np.arange(24) < 5).astype(np.uint8))
     u = np.arange(24, dtype=np.float64).reshape(4, 6)
     assert orc.mask_topk(u, 1)[3, 5] == 1 and orc.mask_topk(u, 1).sum() == 1
+
+
+# ---------------------------------------------------------------- backward
+
+def _grad_case(seed, M, N, K, b_r, b_c, dtype="f32", integers=False):
+    g = np.random.default_rng(seed)
+    if integers:
+        draw = lambda shape: g.integers(-3, 4, shape).astype(np.float32)
+    else:
+        draw = lambda shape: g.normal(0, 1, shape).astype(np.float32)
+    G = wl.quantize(draw((M, N)), dtype)
+    X = wl.quantize(draw((M, K)), dtype)
+    W = wl.quantize(draw((N, K)), dtype)
+    mask = (g.random((N // b_r, K // b_c)) < 0.5).astype(np.uint8)
+    mask[0, 0] = 1
+    return G, X, W, mask
+
+
+def _close(a, b, rtol=1e-12):
+    assert abs(a - b) <= rtol * max(1.0, abs(a), abs(b)), (a, b)
+
+
+def pin_grad_x_adjoint_of_forward(orc):
+    # <dX, V> = <G, V W~^T>: the input gradient is the adjoint of the forward
+    # map, which is pinned on its own (the forward oracle runs with X = V)
+    for (b_r, b_c) in [(16, 32), (32, 16)]:
+        G, X, W, mask = _grad_case(71 + b_r, 9, 96, 64, b_r, b_c)
+        V = np.random.default_rng(72).normal(0, 1, X.shape).astype(np.float32)
+        dX = orc.grad_x(G, W, "f32", b_r, b_c, mask)
+        Y = orc.linear(V, W, "f32", b_r, b_c, mask)
+        _close(float((dX * V.astype(np.float64)).sum()), float((Y * G.astype(np.float64)).sum()))
+
+
+def pin_grad_x_vs_numpy(orc):
+    # dX = G W~ with numpy's product over the numpy-built pruned weight
+    G, X, W, mask = _grad_case(73, 7, 64, 96, 32, 16, dtype="bf16")
+    dX = orc.grad_x(G, W, "bf16", 32, 16, mask)
+    ref = wl.to_f32(G, "bf16").astype(np.float64) @ _pruned_f64(W, "bf16", mask, 32, 16)
+    assert np.allclose(dX, ref, rtol=1e-12, atol=1e-12)
+
+
+def pin_grad_w_vs_numpy(orc):
+    # the kept blocks of numpy's G^T X, in BSR order (rows, then kept columns)
+    for (b_r, b_c) in [(16, 32), (32, 16)]:
+        G, X, W, mask = _grad_case(74 + b_c, 11, 96, 64, b_r, b_c, dtype="f16")
+        dW = orc.grad_w(G, X, "f16", b_r, b_c, mask)
+        full = G.astype(np.float64).T @ X.astype(np.float64)
+        ref = [full[r * b_r:(r + 1) * b_r, c * b_c:(c + 1) * b_c]
+               for r in range(mask.shape[0]) for c in range(mask.shape[1]) if mask[r, c]]
+        assert dW.shape == (len(ref), b_r, b_c)
+        assert np.allclose(dW, np.array(ref), rtol=1e-12, atol=1e-12)
+
+
+def pin_grad_w_adjoint_of_forward(orc):
+    # <dW, U> over the kept blocks = <G, X U~^T>, the forward oracle with weight U
+    G, X, W, mask = _grad_case(75, 13, 64, 96, 16, 32)
+    U = np.random.default_rng(76).normal(0, 1, W.shape).astype(np.float32)
+    dW = orc.grad_w(G, X, "f32", 16, 32, mask)
+    _, _, Ub = orc.pack(U, "f32", 16, 32, mask)
+    Y = orc.linear(X, U, "f32", 16, 32, mask)
+    _close(float((dW * Ub.astype(np.float64)).sum()), float((Y * G.astype(np.float64)).sum()))
+
+
+def pin_grad_bias_adjoint_and_exact(orc):
+    # <db, u> = <G, Y> for the forward oracle with X = 0 and bias u (Y[m] = u);
+    # with integer G every partial sum is exact, so db equals int64 sums
+    G, X, W, mask = _grad_case(77, 10, 64, 32, 16, 16)
+    u = np.random.default_rng(78).normal(0, 1, 64).astype(np.float32)
+    db = orc.grad_bias(G, "f32")
+    Y = orc.linear(np.zeros_like(X), W, "f32", 16, 16, mask, bias=u)
+    _close(float((db * u.astype(np.float64)).sum()), float((Y * G.astype(np.float64)).sum()))
+    Gi, _, _, _ = _grad_case(79, 33, 48, 16, 16, 16, integers=True)
+    assert np.array_equal(orc.grad_bias(Gi, "f32"), Gi.astype(np.int64).sum(axis=0).astype(np.float64))
+
+
+def pin_grad_exact_integers(orc):
+    # small integers: every product and partial sum is exact, so both
+    # gradients equal int64 arithmetic exactly
+    G, X, W, mask = _grad_case(80, 17, 64, 96, 32, 16, integers=True)
+    Wi = np.where(_expand(mask, 32, 16), W.astype(np.int64), 0)
+    assert np.array_equal(orc.grad_x(G, W, "f32", 32, 16, mask),
+                          (G.astype(np.int64) @ Wi).astype(np.float64))
+    full = G.astype(np.int64).T @ X.astype(np.int64)
+    dW = orc.grad_w(G, X, "f32", 32, 16, mask)
+    k = 0
+    for r in range(mask.shape[0]):
+        for c in range(mask.shape[1]):
+            if mask[r, c]:
+                assert np.array_equal(dW[k], full[r * 32:(r + 1) * 32, c * 16:(c + 1) * 16])
+                k += 1
+    assert k == dW.shape[0]
 
 
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

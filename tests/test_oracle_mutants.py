@@ -56,6 +56,21 @@ MUTANTS = {
                          "return ((100 - (int64_t)sparsity_pct) * n_blocks) / 100;"),
     "topk_ties_to_higher": ("return i < j ? -1 : (i > j ? 1 : 0);",
                             "return i < j ? 1 : (i > j ? -1 : 0);"),
+    "gradx_mask_ignored": (
+        "Wd[n * K + k] = mask[(n / b_r) * C + (k / b_c)] ? dec_one(dtype, W, n * ldw + k) : 0.0;",
+        "Wd[n * K + k] = dec_one(dtype, W, n * ldw + k);"),
+    "gradx_rows_reversed": ("const double* wn = j->Wd + n * j->K;",
+                            "const double* wn = j->Wd + (j->N - 1 - n) * j->K;"),
+    "gradx_sign_flipped": ("out[k] += g * wn[k];", "out[k] -= g * wn[k];"),
+    "gradw_block_transposed": ("out[i * b_c + j] += g[i] * x[j];", "out[j * b_r + i] += g[i] * x[j];"),
+    "gradw_last_token_dropped": ("for (int64_t m = 0; m < M; ++m) {\n                    for (int i = 0;",
+                                 "for (int64_t m = 0; m < M - 1; ++m) {\n                    for (int i = 0;"),
+    "gradw_wrong_g_stride": ("g[i] = dec_one(dtype, G, m * ldg + r * b_r + i);",
+                             "g[i] = dec_one(dtype, G, m * ldg + r * b_c + i);"),
+    "gradw_x_from_g": ("x[j] = dec_one(dtype, X, m * ldx + c * b_c + j);",
+                       "x[j] = dec_one(dtype, G, m * ldg + c * b_c + j);"),
+    "gradb_first_row_dropped": ("for (int64_t m = 0; m < M; ++m)\n            s += dec_one(dtype, G, m * ldg + n);",
+                                "for (int64_t m = 1; m < M; ++m)\n            s += dec_one(dtype, G, m * ldg + n);"),
     "topk_keeps_lowest": ("    if (si > sj)\n        return -1;\n    if (si < sj)\n        return 1;",
                           "    if (si > sj)\n        return 1;\n    if (si < sj)\n        return -1;"),
 }
