@@ -202,6 +202,58 @@ lpv_status lpv_mask_topk(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_d
                          int32_t b_r, int32_t b_c, const void* G, int64_t ldg,
                          int32_t sparsity_pct, uint8_t* mask, double* scores, void* stream);
 
+/*
+ * Backward of the layer, for finetuning the pruned model (Fig. 1, Sec. 4).
+ * The mask stays fixed: a dropped block neither passes a gradient to the
+ * input nor receives one.  G is the gradient at the pre-activation
+ * Z = X W~^T + b (M x N): with the GELU epilogue the caller multiplies dL/dY
+ * by GELU'(Z) element-wise first.  The three results follow from the chain
+ * rule: dX = G W~, dW = G^T X on the kept blocks, db = sum over tokens of G.
+ */
+
+/*
+ * lpv_bsr_transpose -- a new handle holding W~^T (K x N, blocks b_c x b_r) of
+ * the handle h, so that the input gradient is the forward call on it:
+ *   lpv_bsr_linear(ht, G, ldg, M, NULL, dX, lddx, LPV_EPI_NONE, stream)
+ * computes dX = G W~ (M x K).  Its BSR arrays are those lpv_bsr_pack gives for
+ * the transposed weight and mask.  Device work on `stream`, synchronised
+ * before returning (like lpv_bsr_pack); temporary device memory of K N
+ * elements is allocated and freed.  *out receives the handle (release it with
+ * lpv_bsr_destroy), NULL on failure.
+ * Errors: INVALID_ARG, SHAPE (K N too large for pack), ALLOC, HIP.
+ */
+lpv_status lpv_bsr_transpose(const lpv_bsr* h, void* stream, lpv_bsr** out);
+
+/*
+ * lpv_bsr_grad_w -- the weight gradient on the kept blocks:
+ *   dW[n][k] = sum over m of G[m][n] X[m][k]   for (n, k) in a kept block.
+ * G       device, M x N (row stride ldg >= N), the handle's element type.
+ * X       device, M x K (row stride ldx >= K), same type: the layer's input.
+ * dW      device, nnzb x b_r x b_c elements of the handle's type, written in
+ *         the BSR value order of lpv_bsr_export (block-rows ascending, kept
+ *         columns ascending, each block row-major).
+ * Sums run in float32 over fixed token chunks added in a fixed order, one
+ * rounding at the end.  16-bit types use the matrix cores; fp32 handles a
+ * plain kernel.  Allocates and frees a stream-ordered workspace (partial sums
+ * of the kept tiles per token chunk).  M = 0 writes zeros.  G, X 16-byte
+ * aligned, ldg and ldx multiples of 16 bytes and at most 2^22 elements,
+ * M < 2^31.  No host synchronisation.
+ * Errors: INVALID_ARG, SHAPE, ALLOC, HIP.
+ */
+lpv_status lpv_bsr_grad_w(const lpv_bsr* h, const void* G, int64_t ldg, const void* X,
+                          int64_t ldx, int64_t M, void* dW, void* stream);
+
+/*
+ * lpv_bias_grad -- db[n] = sum over m of G[m][n] (N elements of type dt).
+ * G device, M x N, row stride ldg >= N, 16-byte aligned, ldg a multiple of 16
+ * bytes.  float32 sums over fixed token chunks added in order, one rounding.
+ * Allocates and frees a stream-ordered workspace; no host synchronisation.
+ * M = 0 gives zeros.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, ALLOC, HIP.
+ */
+lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
+                         void* db, void* stream);
+
 /* Release a handle and its device buffers.  NULL-safe.  The caller must make
  * sure no enqueued work still uses it. */
 void lpv_bsr_destroy(lpv_bsr* h);

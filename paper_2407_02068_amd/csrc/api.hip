@@ -430,6 +430,118 @@ lpv_status lpv_mask_topk(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_d
     return e == hipSuccess ? LPV_OK : hip_fail(e, "mask_topk launch");
 }
 
+lpv_status lpv_bsr_transpose(const lpv_bsr* h, void* stream, lpv_bsr** out)
+{
+    g_err[0] = 0;
+    if (!out)
+        return fail(LPV_ERR_INVALID_ARG, "out must not be NULL");
+    *out = nullptr;
+    if (!h)
+        return fail(LPV_ERR_INVALID_ARG, "handle must not be NULL");
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (dev != h->device)
+        return fail(LPV_ERR_INVALID_ARG, "handle lives on device %d, current device is %d",
+                    h->device, dev);
+    hipStream_t s = (hipStream_t)stream;
+    const int es = elem_size(h->dtype);
+    // the pruned weight transposed (K x N, row stride N) and the transposed
+    // mask (C x R), built on the device and packed like any weight
+    void* WT = nullptr;
+    void* mT = nullptr;
+    e = dmalloc(&WT, (size_t)(h->K * h->N) * es);
+    if (e == hipSuccess)
+        e = dmalloc(&mT, (size_t)h->R * h->C);
+    if (e != hipSuccess) {
+        (void)hipFree(WT);
+        return e == hipErrorOutOfMemory ? fail(LPV_ERR_ALLOC, "device allocation failed")
+                                        : hip_fail(e, "hipMalloc");
+    }
+    e = hipMemsetAsync(WT, 0, (size_t)(h->K * h->N) * es, s);
+    if (e == hipSuccess)
+        e = hipMemsetAsync(mT, 0, (size_t)h->R * h->C, s);
+    if (e == hipSuccess)
+        e = lpv::launch_transpose_blocks(h, WT, h->N, (uint8_t*)mT, s);
+    lpv_status st = e == hipSuccess ? LPV_OK : hip_fail(e, "transpose launch");
+    if (st == LPV_OK)
+        st = lpv_bsr_pack(WT, h->N, h->K, h->N, (lpv_dtype)h->dtype, h->b_c, h->b_r,
+                          (const uint8_t*)mT, stream, out);
+    const hipError_t es2 = hipStreamSynchronize(s);  // before the buffers are freed
+    (void)hipFree(WT);
+    (void)hipFree(mT);
+    if (st == LPV_OK && es2 != hipSuccess) {
+        lpv_bsr_destroy(*out);
+        *out = nullptr;
+        return hip_fail(es2, "transpose");
+    }
+    return st;
+}
+
+lpv_status lpv_bsr_grad_w(const lpv_bsr* h, const void* G, int64_t ldg, const void* X,
+                          int64_t ldx, int64_t M, void* dW, void* stream)
+{
+    if (!h)
+        return fail(LPV_ERR_INVALID_ARG, "handle must not be NULL");
+    const int es = elem_size(h->dtype);
+    if (M < 0 || M >= MAX_M)
+        return fail(LPV_ERR_SHAPE, "M = %lld is out of range [0, 2^31)", (long long)M);
+    if (ldg < h->N || ldx < h->K)
+        return fail(LPV_ERR_INVALID_ARG, "ldg must be >= N and ldx >= K");
+    if (ldg > MAX_LD || ldx > MAX_LD)
+        return fail(LPV_ERR_INVALID_ARG, "ldg and ldx must be at most %lld", (long long)MAX_LD);
+    if ((ldg * es) % 16 || (ldx * es) % 16)
+        return fail(LPV_ERR_INVALID_ARG, "ldg and ldx must be multiples of 16 bytes");
+    if (h->nnzb > 0 && (!dW || (uintptr_t)dW % es))
+        return fail(LPV_ERR_INVALID_ARG, "dW must be non-NULL and aligned to its element size");
+    if (M > 0 && (!G || !X || !aligned16(G) || !aligned16(X)))
+        return fail(LPV_ERR_INVALID_ARG, "G and X must be non-NULL and 16-byte aligned");
+    if (M > 0 && h->nnzb > 0) {
+        const uintptr_t w0 = (uintptr_t)dW,
+                        w1 = w0 + (uintptr_t)(h->nnzb * h->b_r * h->b_c * es);
+        const uintptr_t g0 = (uintptr_t)G, g1 = g0 + (uintptr_t)(((M - 1) * ldg + h->N) * es);
+        const uintptr_t x0 = (uintptr_t)X, x1 = x0 + (uintptr_t)(((M - 1) * ldx + h->K) * es);
+        if ((w0 < g1 && g0 < w1) || (w0 < x1 && x0 < w1))
+            return fail(LPV_ERR_ALIAS, "dW overlaps G or X");
+    }
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return hip_fail(e, "hipGetDevice");
+    if (dev != h->device)
+        return fail(LPV_ERR_INVALID_ARG, "handle lives on device %d, current device is %d",
+                    h->device, dev);
+    lpv::GradWCall c = {G, ldg, X, ldx, M, dW};
+    e = lpv::launch_grad_w(h, c, (hipStream_t)stream);
+    if (e == hipErrorOutOfMemory)
+        return fail(LPV_ERR_ALLOC, "workspace allocation failed");
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "grad_w launch");
+}
+
+lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
+                         void* db, void* stream)
+{
+    const int es = elem_size(dt);
+    if (!es)
+        return fail(LPV_ERR_DTYPE, "unknown element type %d", (int)dt);
+    if (N <= 0 || N > MAX_DIM)
+        return fail(LPV_ERR_SHAPE, "N = %lld is out of range [1, %lld]", (long long)N,
+                    (long long)MAX_DIM);
+    if (M < 0 || M >= MAX_M)
+        return fail(LPV_ERR_SHAPE, "M = %lld is out of range [0, 2^31)", (long long)M);
+    if (ldg < N || ldg > MAX_LD || (ldg * es) % 16)
+        return fail(LPV_ERR_INVALID_ARG, "ldg must be in [N, 2^22] and a multiple of 16 bytes");
+    if (!db || (uintptr_t)db % es)
+        return fail(LPV_ERR_INVALID_ARG, "db must be non-NULL and aligned to its element size");
+    if (M > 0 && (!G || !aligned16(G)))
+        return fail(LPV_ERR_INVALID_ARG, "G must be non-NULL and 16-byte aligned");
+    hipError_t e = lpv::launch_bias_grad(G, ldg, M, N, dt, db, (hipStream_t)stream);
+    if (e == hipErrorOutOfMemory)
+        return fail(LPV_ERR_ALLOC, "workspace allocation failed");
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "bias_grad launch");
+}
+
 void lpv_bsr_destroy(lpv_bsr* h)
 {
     free_handle(h);

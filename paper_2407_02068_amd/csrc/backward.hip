@@ -1,0 +1,561 @@
+// backward.hip -- backward of the block-sparse linear layer, for finetuning
+// the pruned model (gfx950).
+//
+// Paper, Fig. 1 and Sec. 4: after block pruning the model is finetuned.  The
+// mask stays fixed: a dropped block is absent from the layer, so it neither
+// passes a gradient to the input nor receives one.  For the pre-activation
+// Z = X W~^T + b and G = dL/dZ (M x N):
+//   dX = G W~         the forward kernel run on the handle of W~^T, which
+//                     k_transpose_blocks + pack build (lpv_bsr_transpose)
+//   dW = G^T X        on the kept blocks only: k_gradw_tiles (matrix cores)
+//                     and k_gradw_reduce, or k_gradw_plain for fp32 handles
+//   db = sum_m G[m]   k_bias_partial + k_bias_reduce
+// Every sum is taken in a fixed order, so results do not depend on timing.
+#include "lpv_device.h"
+#include "lpv_internal.h"
+
+namespace lpv {
+namespace {
+
+static __device__ uint4 g_zero_line[1];
+
+// ---------------------------------------------------------------- transpose
+
+// One workgroup per block-row r: every kept block (r, c) of the handle is
+// written transposed into the dense K x N buffer WT (block (c, r) of W~^T),
+// and maskT[c][r] is set.  Everything else in WT and maskT is left as the
+// caller cleared it.
+__global__ __launch_bounds__(256) void k_transpose_blocks(int32_t b_r, int32_t b_c, int32_t R,
+                                                          int32_t es, const int32_t* __restrict__ row_ptr,
+                                                          const int32_t* __restrict__ col_idx,
+                                                          const char* __restrict__ values,
+                                                          char* __restrict__ WT, int64_t ldwt,
+                                                          uint8_t* __restrict__ maskT)
+{
+    const int r = blockIdx.x;
+    const int p0 = row_ptr[r], p1 = row_ptr[r + 1];
+    const int nb = b_r * b_c;
+    for (int p = p0; p < p1; ++p) {
+        const int c = col_idx[p];
+        if (threadIdx.x == 0)
+            maskT[(int64_t)c * R + r] = 1;
+        for (int e = threadIdx.x; e < nb; e += 256) {
+            const int i = e / b_c, j = e - i * b_c;  // W~[r b_r + i][c b_c + j]
+            const char* src = values + ((int64_t)p * nb + e) * es;
+            char* dst = WT + (((int64_t)c * b_c + j) * ldwt + (int64_t)r * b_r + i) * es;
+            if (es == 4)
+                *(uint32_t*)dst = *(const uint32_t*)src;
+            else
+                *(uint16_t*)dst = *(const uint16_t*)src;
+        }
+    }
+}
+
+// ---------------------------------------------------------------- element access
+
+template <int DT> __device__ inline float load_elem(const char* base, int64_t idx)
+{
+    if constexpr (DT == LPV_F32)
+        return ((const float*)base)[idx];
+    else
+        return Elem<DT>::to_f32(((const uint16_t*)base)[idx]);
+}
+
+template <int DT> __device__ inline void store_elem(char* base, int64_t idx, float v)
+{
+    if constexpr (DT == LPV_F32)
+        ((float*)base)[idx] = v;
+    else
+        ((uint16_t*)base)[idx] = Elem<DT>::from_f32(v);
+}
+
+// ---------------------------------------------------------------- bias gradient
+
+// part[chunk][n] = sum over the chunk's token rows (ascending) of G[m][n], in
+// float32.  Thread: 16 bytes of columns; grid (column blocks, chunks).
+template <int DT>
+__global__ __launch_bounds__(256) void k_bias_partial(const char* __restrict__ G, int64_t ldg,
+                                                      int64_t M, int64_t N, int64_t rows,
+                                                      float* __restrict__ part)
+{
+    constexpr int ES = DT == LPV_F32 ? 4 : 2, V = 16 / ES;
+    const int64_t n0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * V;
+    const int64_t m0 = (int64_t)blockIdx.y * rows, m1 = min(M, m0 + rows);
+    if (n0 >= N)
+        return;
+    float acc[V];
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+        acc[i] = 0.0f;
+    const bool full = n0 + V <= N;
+    for (int64_t m = m0; m < m1; ++m) {
+        if (full) {
+            const uint4 v = *(const uint4*)(G + (m * ldg + n0) * ES);
+#pragma unroll
+            for (int i = 0; i < V; ++i)
+                acc[i] += load_elem<DT>((const char*)&v, i);
+        } else {
+            for (int i = 0; i < V; ++i)
+                if (n0 + i < N)
+                    acc[i] += load_elem<DT>(G, m * ldg + n0 + i);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < V; ++i)
+        if (n0 + i < N)
+            part[blockIdx.y * N + n0 + i] = acc[i];
+}
+
+// db[n] = the chunks' partial sums added in chunk order, rounded once.
+template <int DT>
+__global__ __launch_bounds__(256) void k_bias_reduce(const float* __restrict__ part, int n_chunks,
+                                                     int64_t N, char* __restrict__ db)
+{
+    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (n >= N)
+        return;
+    float s = 0.0f;
+    for (int c = 0; c < n_chunks; ++c)
+        s += part[c * N + n];
+    store_elem<DT>(db, n, s);
+}
+
+// ---------------------------------------------------------------- weight gradient, fp32
+
+// Block-row of kept block p (row_ptr is ascending).
+__device__ inline int block_row(const int32_t* row_ptr, int R, int64_t p)
+{
+    int lo = 0, hi = R;
+    while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (row_ptr[mid] <= p)
+            lo = mid;
+        else
+            hi = mid;
+    }
+    return lo;
+}
+
+// One workgroup per kept block; each thread sums whole elements over all
+// tokens, ascending.  For fp32 handles (small layers).
+template <int DT>
+__global__ __launch_bounds__(256) void k_gradw_plain(int32_t b_r, int32_t b_c, int32_t R,
+                                                     const int32_t* __restrict__ row_ptr,
+                                                     const int32_t* __restrict__ col_idx,
+                                                     const char* __restrict__ G, int64_t ldg,
+                                                     const char* __restrict__ X, int64_t ldx,
+                                                     int64_t M, char* __restrict__ out)
+{
+    const int64_t p = blockIdx.x;
+    const int r = block_row(row_ptr, R, p), c = col_idx[p];
+    const int nb = b_r * b_c;
+    for (int e = threadIdx.x; e < nb; e += 256) {
+        const int i = e / b_c, j = e - i * b_c;
+        const int64_t n = (int64_t)r * b_r + i, k = (int64_t)c * b_c + j;
+        float acc = 0.0f;
+        for (int64_t m = 0; m < M; ++m)
+            acc += load_elem<DT>(G, m * ldg + n) * load_elem<DT>(X, m * ldx + k);
+        store_elem<DT>(out, p * nb + e, acc);
+    }
+}
+
+// ---------------------------------------------------------------- weight gradient, 16-bit
+
+// A workgroup takes a *window* -- one schedule group (8 tile rows, 256
+// outputs n) times 8 tile columns (256 inputs k) -- and a chunk of tokens, and
+// computes for every kept 32 x 32 tile of the window the partial product
+// G[chunk, tile rows]^T X[chunk, tile columns] with the matrix cores.  Tokens
+// are the reduction: they stream through a 4-stage LDS ring, 32 per stage
+// (G: 32 x 256 and X: 32 x 256 elements, 16 KB each, rows of 512 bytes whose
+// 64-byte segments are XOR-swizzled by the row).  The MFMA operands need 8
+// consecutive tokens per lane; ds_read_b64_tr_b16 gathers them from the
+// token-major rows: within each 16-lane group, lane i receives element i % 4
+// of the 8-byte pieces read by lanes i / 4 + 4 q (q = 0..3), so when lane j
+// reads row t0 + j / 4 at column c0 + 4 (j % 4), lane i holds rows t0 .. t0 + 3
+// of column c0 + i.
+//
+// The window's kept tiles, in row-major order, are dealt to the 8 waves in
+// contiguous runs (at most 8 each, balanced to within one); a run's tiles
+// mostly share a tile row, whose G fragment is then read once per k-step.  A
+// wave reads the operands of its next tile while the current one multiplies.
+// Partials go to ws[chunk][tile row][tile col][1024] in accumulator order
+// (lane-major float4 runs); k_gradw_reduce adds the chunks in order.
+constexpr int GW_NT = 512;
+constexpr int GW_STAGE = 32768;  // bytes: G 16 KB + X 16 KB
+constexpr int GW_NSTG = 4;
+
+struct GradWDims {
+    int64_t M, ldg, ldx, N, K;
+    int32_t n_tile_rows, n_tile_cols, n_groups, n_wcols;
+    int64_t chunk_rows;
+    int32_t n_chunks;
+};
+
+__device__ inline int gw_swz(int row) { return (row & 3) | ((row >> 1) & 4); }
+
+__device__ inline uint32_t lds_u32(const void* p)
+{
+    return (uint32_t)(uintptr_t)((const __attribute__((address_space(3))) char*)p);
+}
+
+// 16 bytes per lane from a per-lane global address into LDS at M0 + 16 lane.
+__device__ inline void gw_dma(const void* src, uint32_t m0)
+{
+    asm volatile(
+        "s_nop 0\n"
+        "global_load_lds_dwordx4 %0, off"
+        :
+        : "v"(src), "{m0}"(m0)
+        : "memory");
+}
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+__device__ inline v4s tr_read(uint32_t addr)
+{
+    return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) v4s*)(uintptr_t)addr);
+}
+
+template <int DT>
+__global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
+                                                          const int32_t* __restrict__ step_ptr,
+                                                          const int32_t* __restrict__ step_col,
+                                                          const int32_t* __restrict__ step_bits,
+                                                          const char* __restrict__ G,
+                                                          const char* __restrict__ X,
+                                                          float* __restrict__ ws)
+{
+    using E = Elem<DT>;
+    using F = typename E::frag;
+    __shared__ uint4 smem[GW_NSTG * GW_STAGE / 16];
+    __shared__ uint32_t s_mask[2];
+
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n_win = d.n_groups * d.n_wcols;
+    const int g = (int)(blockIdx.x % d.n_groups);
+    const int wc = (int)((blockIdx.x / d.n_groups) % d.n_wcols);
+    const int chunk = (int)(blockIdx.x / n_win);
+    const int64_t m_begin = (int64_t)chunk * d.chunk_rows;
+    const int64_t m_end = min(d.M, m_begin + d.chunk_rows);
+
+    // the window's kept tiles: bit 8 j + c for tile row j, tile column c
+    if (tid < 64) {
+        uint64_t bits = 0;
+        const int s0 = step_ptr[g], s1 = step_ptr[g + 1];
+        for (int s = s0 + lane; s < s1; s += 64) {
+            const int c = step_col[s] - 8 * wc;
+            if (c >= 0 && c < 8) {
+                const int rb = step_bits[s];
+#pragma unroll
+                for (int j = 0; j < 8; ++j)
+                    if ((rb >> j) & 1)
+                        bits |= (uint64_t)1 << (8 * j + c);
+            }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const uint32_t lo = __shfl_xor((uint32_t)bits, o, 64);
+            const uint32_t hi = __shfl_xor((uint32_t)(bits >> 32), o, 64);
+            bits |= (uint64_t)lo | ((uint64_t)hi << 32);
+        }
+        if (lane == 0) {
+            s_mask[0] = (uint32_t)bits;
+            s_mask[1] = (uint32_t)(bits >> 32);
+        }
+    }
+    __syncthreads();
+    const uint64_t wmask = (uint64_t)__builtin_amdgcn_readfirstlane(s_mask[0]) |
+                           ((uint64_t)__builtin_amdgcn_readfirstlane(s_mask[1]) << 32);
+    const int n_kept = __popcll(wmask);
+    if (n_kept == 0 || m_begin >= m_end)
+        return;  // uniform for the whole workgroup
+    // this wave's run of tiles
+    const int lo = wave * n_kept / 8, n_w = (wave + 1) * n_kept / 8 - lo;
+    uint64_t rest = wmask;
+    for (int i = 0; i < lo; ++i)
+        rest &= rest - 1;
+    int tj[8], tc[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        tj[t] = 0;
+        tc[t] = 0;
+        if (t < n_w) {
+            const int p = __builtin_ctzll(rest);
+            tj[t] = p >> 3;
+            tc[t] = p & 7;
+            rest &= rest - 1;
+        }
+    }
+
+    // DMA: wave w fills rows 4w .. 4w + 3 of the G and the X part of a stage
+    // (two 1 KB instructions each); LDS chunk q (16 bytes) of row r holds
+    // columns 32 (seg ^ swz(r)) + 8 (q % 4) .. + 7 with seg = q / 4.
+    const uint32_t smem0 = lds_u32(smem);
+    int drow[2];
+    int64_t gcol[2], xcol[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+        drow[i] = 4 * wave + 2 * i + (lane >> 5);
+        const int q = lane & 31;
+        const int col = 32 * ((q >> 2) ^ gw_swz(drow[i])) + 8 * (q & 3);
+        gcol[i] = min((int64_t)g * 256 + col, d.N - 8);  // past the edge: any valid
+        xcol[i] = min((int64_t)wc * 256 + col, d.K - 8);  // columns (never kept)
+    }
+    const int64_t n_steps = (m_end - m_begin + 31) / 32;
+    // issue the DMA of token step st into its stage
+    auto dma_step = [&](int64_t st) {
+        const uint32_t base = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE + (uint32_t)wave * 2048;
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int64_t m = m_begin + st * 32 + drow[i];
+            const char* gs = m < m_end ? G + (m * d.ldg + gcol[i]) * 2 : (const char*)g_zero_line;
+            const char* xs = X + (min(m, d.M - 1) * d.ldx + xcol[i]) * 2;
+            gw_dma(gs, base + i * 1024);
+            gw_dma(xs, base + 16384 + i * 1024);
+        }
+    };
+
+    // transposed operand reads: (k-step ks, half h) -> row and byte offset
+    // within the row; the segment is the tile row (G) or tile column (X)
+    uint32_t roff[2][2], rswz[2][2];
+    {
+        const int q16 = lane >> 4, j16 = lane & 15;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int row = ks * 16 + 8 * (q16 >> 1) + 4 * h + (j16 >> 2);
+                roff[ks][h] = (uint32_t)(row * 512 + 32 * (q16 & 1) + 8 * (j16 & 3));
+                rswz[ks][h] = (uint32_t)(gw_swz(row) << 6);
+            }
+    }
+    auto frag = [&](uint32_t stage, int ks, int seg) {
+        const uint32_t s6 = (uint32_t)seg << 6;
+        const v4s lo4 = tr_read(stage + roff[ks][0] + (s6 ^ rswz[ks][0]));
+        const v4s hi4 = tr_read(stage + roff[ks][1] + (s6 ^ rswz[ks][1]));
+        const v4s both[2] = {lo4, hi4};
+        return __builtin_bit_cast(F, both);
+    };
+
+    f32x16 acc[8];
+#pragma unroll
+    for (int t = 0; t < 8; ++t)
+        acc[t] = f32x16{};
+
+    // prologue: steps 0, 1, 2
+    for (int64_t st = 0; st < 3 && st < n_steps; ++st)
+        dma_step(st);
+    for (int64_t st = 0; st < n_steps; ++st) {
+        // step st has landed for this wave once at most the DMA of the steps
+        // after it (4 instructions each) is in flight; then the barrier
+        // publishes it to everyone and frees the stage of step st - 1
+        const int64_t ahead = min((int64_t)2, n_steps - 1 - st);
+        if (ahead == 2)
+            asm volatile("s_waitcnt vmcnt(8)\n s_barrier" ::: "memory");
+        else if (ahead == 1)
+            asm volatile("s_waitcnt vmcnt(4)\n s_barrier" ::: "memory");
+        else
+            asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory");
+        if (st + 3 < n_steps)
+            dma_step(st + 3);
+        const uint32_t stage = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE;
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+            // the operands of tile t + 1 are read while tile t multiplies
+            F a = frag(stage, ks, tj[0]);
+            F b = frag(stage + 16384, ks, tc[0]);
+#pragma unroll
+            for (int t = 0; t < 8; ++t) {
+                if (t < n_w) {
+                    F an = a, bn = b;
+                    if (t + 1 < n_w) {
+                        if (tj[t + 1] != tj[t])
+                            an = frag(stage, ks, tj[t + 1]);
+                        bn = frag(stage + 16384, ks, tc[t + 1]);
+                    }
+                    acc[t] = E::mma(a, b, acc[t]);
+                    a = an;
+                    b = bn;
+                }
+            }
+        }
+    }
+
+    // partials of this chunk
+#pragma unroll
+    for (int t = 0; t < 8; ++t) {
+        if (t < n_w) {
+            const int64_t tile = (int64_t)(8 * g + tj[t]) * d.n_tile_cols + (8 * wc + tc[t]);
+            float* dst = ws + ((int64_t)chunk * d.n_tile_rows * d.n_tile_cols + tile) * 1024;
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                const float4 v = {acc[t][4 * qq], acc[t][4 * qq + 1], acc[t][4 * qq + 2],
+                                  acc[t][4 * qq + 3]};
+                *(float4*)(dst + qq * 256 + lane * 4) = v;
+            }
+        }
+    }
+}
+
+// out[p][i][j] (BSR order) = the chunks' partials of element (n, k) =
+// (r b_r + i, c b_c + j) added in chunk order, rounded once.  Accumulator
+// order inside a 32 x 32 tile: element (nn, kk) is lane kk + 32 ((nn / 4) % 2),
+// register 4 (nn / 8) + nn % 4.
+template <int DT>
+__global__ __launch_bounds__(256) void k_gradw_reduce(int32_t b_r, int32_t b_c, int32_t R,
+                                                      const int32_t* __restrict__ row_ptr,
+                                                      const int32_t* __restrict__ col_idx,
+                                                      int64_t total, int32_t n_tile_cols,
+                                                      int64_t chunk_stride, int32_t n_chunks,
+                                                      const float* __restrict__ ws,
+                                                      char* __restrict__ out)
+{
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= total)
+        return;
+    const int nb = b_r * b_c;
+    const int64_t p = idx / nb;
+    const int e = (int)(idx - p * nb);
+    const int r = block_row(row_ptr, R, p), c = col_idx[p];
+    const int i = e / b_c, j = e - i * b_c;
+    const int64_t n = (int64_t)r * b_r + i, k = (int64_t)c * b_c + j;
+    const int nn = (int)(n & 31), kk = (int)(k & 31);
+    const int64_t off = ((n >> 5) * n_tile_cols + (k >> 5)) * 1024 + (nn >> 3) * 256 +
+                        (kk + 32 * ((nn >> 2) & 1)) * 4 + (nn & 3);
+    float s = 0.0f;
+    for (int ch = 0; ch < n_chunks; ++ch)
+        s += ws[ch * chunk_stride + off];
+    store_elem<DT>(out, idx, s);
+}
+
+int device_cus()
+{
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+        return 256;
+    return n;
+}
+
+}  // namespace
+
+hipError_t launch_transpose_blocks(const lpv_bsr* h, void* WT, int64_t ldwt, uint8_t* maskT,
+                                   hipStream_t s)
+{
+    const int es = h->dtype == LPV_F32 ? 4 : 2;
+    if (h->R > 0)
+        hipLaunchKernelGGL(k_transpose_blocks, dim3(h->R), dim3(256), 0, s, h->b_r, h->b_c, h->R,
+                           es, (const int32_t*)h->row_ptr, (const int32_t*)h->col_idx,
+                           (const char*)h->values, (char*)WT, ldwt, maskT);
+    return hipGetLastError();
+}
+
+hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype, void* db,
+                            hipStream_t s)
+{
+    const int V = dtype == LPV_F32 ? 4 : 8;
+    const int64_t bx = (N + 256 * V - 1) / (256 * V);
+    int64_t n_chunks = (2048 + bx - 1) / bx;
+    n_chunks = max((int64_t)1, min(n_chunks, (M + 63) / 64));
+    const int64_t rows = (M + n_chunks - 1) / n_chunks;
+    n_chunks = M > 0 ? (M + rows - 1) / rows : 1;
+    float* part = nullptr;
+    hipError_t e = hipMallocAsync((void**)&part, (size_t)(n_chunks * N) * sizeof(float), s);
+    if (e != hipSuccess)
+        return e;
+    if (M > 0) {
+#define LPV_BIAS(DT_)                                                                            \
+    hipLaunchKernelGGL(k_bias_partial<DT_>, dim3((unsigned)bx, (unsigned)n_chunks), dim3(256), 0, \
+                       s, (const char*)G, ldg, M, N, rows, part)
+        if (dtype == LPV_BF16)
+            LPV_BIAS(LPV_BF16);
+        else if (dtype == LPV_F16)
+            LPV_BIAS(LPV_F16);
+        else
+            LPV_BIAS(LPV_F32);
+#undef LPV_BIAS
+    } else {
+        n_chunks = 0;  // no tokens: db = 0
+    }
+    e = hipGetLastError();
+    if (e == hipSuccess) {
+        const dim3 grid((unsigned)((N + 255) / 256));
+        if (dtype == LPV_BF16)
+            hipLaunchKernelGGL(k_bias_reduce<LPV_BF16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
+        else if (dtype == LPV_F16)
+            hipLaunchKernelGGL(k_bias_reduce<LPV_F16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
+        else
+            hipLaunchKernelGGL(k_bias_reduce<LPV_F32>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
+        e = hipGetLastError();
+    }
+    const hipError_t ef = hipFreeAsync(part, s);
+    return e != hipSuccess ? e : ef;
+}
+
+hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
+{
+    if (h->nnzb == 0)
+        return hipSuccess;
+    const int64_t nb = (int64_t)h->b_r * h->b_c;
+    const int64_t total = h->nnzb * nb;
+    if (c.M == 0) {
+        // no tokens: every kept-block gradient is zero
+        return hipMemsetAsync(c.dW, 0, (size_t)total * (h->dtype == LPV_F32 ? 4 : 2), s);
+    }
+    if (h->dtype == LPV_F32) {
+        hipLaunchKernelGGL(k_gradw_plain<LPV_F32>, dim3((unsigned)h->nnzb), dim3(256), 0, s, h->b_r,
+                           h->b_c, h->R, (const int32_t*)h->row_ptr, (const int32_t*)h->col_idx,
+                           (const char*)c.G, c.ldg, (const char*)c.X, c.ldx, c.M, (char*)c.dW);
+        return hipGetLastError();
+    }
+    GradWDims d = {};
+    d.M = c.M;
+    d.ldg = c.ldg;
+    d.ldx = c.ldx;
+    d.N = h->N;
+    d.K = h->K;
+    d.n_tile_rows = h->n_tile_rows;
+    d.n_tile_cols = h->n_tile_cols;
+    d.n_groups = h->n_groups;
+    d.n_wcols = (h->n_tile_cols + 7) / 8;
+    const int64_t n_win = (int64_t)d.n_groups * d.n_wcols;
+    // about one workgroup per compute unit; chunks of whole 32-token steps
+    int64_t n_chunks = max((int64_t)1, (int64_t)device_cus() / n_win);
+    n_chunks = min(n_chunks, (c.M + 31) / 32);
+    d.chunk_rows = ((c.M + n_chunks - 1) / n_chunks + 31) / 32 * 32;
+    d.n_chunks = (int32_t)((c.M + d.chunk_rows - 1) / d.chunk_rows);
+    const int64_t chunk_stride = (int64_t)d.n_tile_rows * d.n_tile_cols * 1024;
+    float* ws = nullptr;
+    hipError_t e = hipMallocAsync((void**)&ws, (size_t)(d.n_chunks * chunk_stride) * sizeof(float), s);
+    if (e != hipSuccess)
+        return e;
+    const dim3 grid((unsigned)(n_win * d.n_chunks)), block(GW_NT);
+    const dim3 rgrid((unsigned)((total + 255) / 256));
+    if (h->dtype == LPV_BF16) {
+        hipLaunchKernelGGL(k_gradw_tiles<LPV_BF16>, grid, block, 0, s, d, (const int32_t*)h->step_ptr,
+                           (const int32_t*)h->step_col, (const int32_t*)h->step_bits,
+                           (const char*)c.G, (const char*)c.X, ws);
+        e = hipGetLastError();
+        if (e == hipSuccess)
+            hipLaunchKernelGGL(k_gradw_reduce<LPV_BF16>, rgrid, dim3(256), 0, s, h->b_r, h->b_c,
+                               h->R, (const int32_t*)h->row_ptr, (const int32_t*)h->col_idx,
+                               total, d.n_tile_cols, chunk_stride, d.n_chunks, ws, (char*)c.dW);
+    } else {
+        hipLaunchKernelGGL(k_gradw_tiles<LPV_F16>, grid, block, 0, s, d, (const int32_t*)h->step_ptr,
+                           (const int32_t*)h->step_col, (const int32_t*)h->step_bits,
+                           (const char*)c.G, (const char*)c.X, ws);
+        e = hipGetLastError();
+        if (e == hipSuccess)
+            hipLaunchKernelGGL(k_gradw_reduce<LPV_F16>, rgrid, dim3(256), 0, s, h->b_r, h->b_c,
+                               h->R, (const int32_t*)h->row_ptr, (const int32_t*)h->col_idx,
+                               total, d.n_tile_cols, chunk_stride, d.n_chunks, ws, (char*)c.dW);
+    }
+    if (e == hipSuccess)
+        e = hipGetLastError();
+    const hipError_t ef = hipFreeAsync(ws, s);
+    return e != hipSuccess ? e : ef;
+}
+
+}  // namespace lpv

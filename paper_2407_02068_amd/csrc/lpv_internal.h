@@ -95,4 +95,18 @@ struct MaskCall {
 };
 hipError_t launch_mask_topk(const MaskCall& m, hipStream_t s);
 
+// backward.hip
+struct GradWCall {
+    const void* G;  // M x N, row stride ldg
+    int64_t ldg;
+    const void* X;  // M x K, row stride ldx
+    int64_t ldx, M;
+    void* dW;  // nnzb x b_r x b_c, BSR order
+};
+hipError_t launch_transpose_blocks(const lpv_bsr* h, void* WT, int64_t ldwt, uint8_t* maskT,
+                                   hipStream_t s);
+hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s);
+hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype, void* db,
+                            hipStream_t s);
+
 }  // namespace lpv

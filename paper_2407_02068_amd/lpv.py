@@ -21,6 +21,7 @@ DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 EPI = {None: 0, "none": 0, "gelu": 1}
 EXPORTED = ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
             "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
+            "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad",
             "lpv_bsr_destroy", "lpv_status_str", "lpv_last_error")
 
 
@@ -63,8 +64,12 @@ def lib():
     L.lpv_bsr_linear.argtypes = [vp, vp, i64, i64, vp, vp, i64, i32, vp]
     L.lpv_dense_linear.argtypes = [vp, i64, i64, i64, i32, vp, i64, i64, vp, vp, i64, i32, vp]
     L.lpv_mask_topk.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, i32, vp, vp, vp]
+    L.lpv_bsr_transpose.argtypes = [vp, vp, ctypes.POINTER(vp)]
+    L.lpv_bsr_grad_w.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
+    L.lpv_bias_grad.argtypes = [vp, i64, i64, i64, i32, vp, vp]
     for f in ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
-              "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk"):
+              "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
+              "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad"):
         getattr(L, f).restype = i32
     L.lpv_bsr_destroy.argtypes = [vp]
     L.lpv_bsr_destroy.restype = None
@@ -276,3 +281,45 @@ def mask_topk(W, b_r, b_c, sparsity_pct, G=None, stream=None):
                                ctypes.c_void_p(scores.data_ptr()), _stream(stream)),
            "lpv_mask_topk")
     return mask, scores
+
+
+def bsr_transpose(h, stream=None):
+    """lpv_bsr_transpose: the handle of W~^T (K x N).  The input gradient of the
+    layer is then ``bsr_linear(ht, G)`` = G W~.  Waits for the build."""
+    out = ctypes.c_void_p()
+    _check(lib().lpv_bsr_transpose(h.handle, _stream(stream), ctypes.byref(out)),
+           "lpv_bsr_transpose")
+    return BsrWeight(out.value)
+
+
+def grad_w(h, G, X, out=None, stream=None):
+    """lpv_bsr_grad_w: G^T X on the kept blocks, [nnzb, b_r, b_c] in BSR value
+    order (G: M x N, X: M x K, the handle's dtype)."""
+    if G.dtype != h.dtype or X.dtype != h.dtype:
+        raise TypeError("G and X must be %s" % h.dtype)
+    if G.dim() != 2 or X.dim() != 2 or G.shape[0] != X.shape[0] \
+            or G.shape[1] != h.info["N"] or X.shape[1] != h.info["K"]:
+        raise ValueError("G must be M x %d and X M x %d" % (h.info["N"], h.info["K"]))
+    shape = (h.info["nnzb"], h.info["b_r"], h.info["b_c"])
+    if out is None:
+        out = torch.empty(shape, dtype=h.dtype, device=G.device)
+    if out.dtype != h.dtype or tuple(out.shape) != shape or not out.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor of shape %s" % (h.dtype, shape))
+    gp, ldg = _mat(G, "G")
+    xp, ldx = _mat(X, "X")
+    _check(lib().lpv_bsr_grad_w(h.handle, gp, ldg, xp, ldx, G.shape[0],
+                                ctypes.c_void_p(out.data_ptr()), _stream(stream)), "lpv_bsr_grad_w")
+    return out
+
+
+def bias_grad(G, out=None, stream=None):
+    """lpv_bias_grad: the column sums of G (M x N) -> N elements of G's dtype."""
+    gp, ldg = _mat(G, "G")
+    M, N = G.shape
+    if out is None:
+        out = torch.empty(N, dtype=G.dtype, device=G.device)
+    if out.dtype != G.dtype or out.numel() != N or not out.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor of %d elements" % (G.dtype, N))
+    _check(lib().lpv_bias_grad(gp, ldg, M, N, DTYPES[G.dtype], ctypes.c_void_p(out.data_ptr()),
+                               _stream(stream)), "lpv_bias_grad")
+    return out

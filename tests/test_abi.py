@@ -143,3 +143,20 @@ def mask_topk(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, b_r=32, b_c=32, G=0, ldg=
 def test_mask_topk_rejects_bad_arguments(L, kw, want):
     assert mask_topk(L, **kw) == want
     assert L.lpv_last_error().decode() != ""
+
+
+def test_backward_rejects_bad_arguments(L):
+    out = ctypes.c_void_p(123)
+    assert L.lpv_bsr_transpose(None, None, ctypes.byref(out)) == INVALID and out.value is None
+    assert L.lpv_bsr_transpose(None, None, None) == INVALID
+    assert L.lpv_bsr_grad_w(None, FAKE, 3072, FAKE, 768, 10, FAKE, None) == INVALID
+    # bias gradient: every check runs before any HIP call
+    bg = lambda G=FAKE, ldg=3072, M=10, N=3072, dt=2, db=FAKE + (1 << 32): \
+        L.lpv_bias_grad(G, ldg, M, N, dt, db, None)
+    assert bg(dt=7) == DTYPE
+    assert bg(N=0) == SHAPE and bg(N=1 << 17) == SHAPE
+    assert bg(M=-1) == SHAPE and bg(M=1 << 31) == SHAPE
+    assert bg(ldg=3000) == INVALID and bg(ldg=3076) == INVALID and bg(ldg=(1 << 22) + 8) == INVALID
+    assert bg(db=0) == INVALID and bg(db=FAKE + 1) == INVALID
+    assert bg(G=0) == INVALID and bg(G=FAKE + 8) == INVALID
+    assert L.lpv_last_error().decode() != ""

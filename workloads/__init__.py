@@ -24,7 +24,7 @@ from typing import List, Optional
 import numpy as np
 
 SEED_ROOT = 240702068
-T_X, T_W, T_BIAS, T_MASK, T_SPARSITY, T_ZIPF = range(6)
+T_X, T_W, T_BIAS, T_MASK, T_SPARSITY, T_ZIPF, T_GRAD = range(7)
 TOKENS_PER_IMAGE = 197  # 224x224 image, 16x16 patches, plus the class token
 
 
@@ -277,6 +277,12 @@ def b_stack(M=256 * TOKENS_PER_IMAGE, layers=12, zipf_s=1.0):
 
 FC1_SWEEP_BLOCKS = (16, 32, 64)
 FC1_SWEEP_SPARSITY = (0, 25, 50, 75, 90)
+
+
+def grad_output(cfg, layer, M, N, dtype):
+    """The backward's input: a gradient at the layer's pre-activation, M x N,
+    N(0, 1) rounded to the element type (no trained loss exists here)."""
+    return quantize(rng(cfg, layer, T_GRAD).standard_normal((M, N), dtype=np.float32), dtype)
 
 
 def b_fc1(block=32, sparsity=50, dtype="bf16", M=256 * TOKENS_PER_IMAGE, gelu=False, with_x=True):
