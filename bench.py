@@ -223,6 +223,42 @@ def time_flushed(fn, steps, flush_buf):
     return sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
 
 
+def time_backward(w, h, W, X, steps, tt, to_dev):
+    """The layer's backward at the same workload (finetuning): dX = G W~ by the
+    forward kernel on the transposed handle, dW = G^T X on the kept blocks,
+    db = the column sums of G; G is a seeded N(0, 1) gradient.  Dense
+    references: the library's dense kernel for dX (on W~^T) and hipBLASLt's
+    full G^T X for dW."""
+    import torch
+
+    import workloads as wl
+    from paper_2407_02068_amd import lpv
+    G = to_dev(wl.grad_output(4, 0, w.M, w.N, w.dtype))
+    ht = lpv.bsr_transpose(h)
+    dX = torch.empty((w.M, w.K), dtype=tt, device="cuda")
+    dXd = torch.empty_like(dX)
+    dW = torch.empty((w.nnzb, w.b_r, w.b_c), dtype=tt, device="cuda")
+    db = torch.empty(w.N, dtype=tt, device="cuda")
+    WT = lpv.bsr_unpack(h).t().contiguous()        # W~^T, K x N, for the dense dX
+    Gt = G.t().contiguous()                        # for hipBLASLt's G^T X
+    steps = max(10, steps // 2)
+    _, xms = time_launches(lambda: lpv.bsr_linear(ht, G, None, dX), steps, 10)
+    _, xdms = time_launches(lambda: lpv.dense_linear(WT, G, None, dXd), steps, 10)
+    _, wms = time_launches(lambda: lpv.grad_w(h, G, X, dW), steps, 10)
+    _, wbms = time_launches(lambda: torch.mm(Gt, X), steps, 5)
+    _, bms = time_launches(lambda: lpv.bias_grad(G, db), steps, 10)
+    ht.close()
+    kept = w.kept_flops()
+    avg = lambda ms: sum(ms) / len(ms)
+    return {"dx_ms": round(avg(xms), 5), "dx_dense_ms": round(avg(xdms), 5),
+            "dx_tflops": round(kept / (avg(xms) * 1e-3) / 1e12, 1),
+            "dw_ms": round(avg(wms), 5), "dw_tflops": round(kept / (avg(wms) * 1e-3) / 1e12, 1),
+            "dw_frac_of_peak": round(kept / (avg(wms) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+            "dw_hipblaslt_dense_ms": round(avg(wbms), 5), "db_ms": round(avg(bms), 5),
+            "note": "event averages; dW includes its stream-ordered workspace and chunk "
+                    "reduction; G seeded N(0, 1)"}
+
+
 def pct(ms, q):
     return ms[min(len(ms) - 1, int(q * (len(ms) - 1) + 0.5))]
 
@@ -263,6 +299,7 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-backward", action="store_true", help="skip the backward timings")
     ap.add_argument("--no-flushed", action="store_true",
                     help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
@@ -347,6 +384,7 @@ def main():
     # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
     bl = lambda: torch.addmm(b, X, W.t())
     _, bms = time_launches(bl, max(5, args.steps // 2), 3)
+    back = None if args.no_backward else time_backward(w, h, W, X, args.steps, tt, to_dev)
     # cold caches: the same launches after a 1 GiB write each
     fms = fdms = None
     if not args.no_flushed:
@@ -369,6 +407,10 @@ def main():
         % (pct(ms, .5) * 1e3, pct(ms, .1) * 1e3, pct(ms, .9) * 1e3, achieved, hbm_gbs))
     log("dense_linear: median %.1f us, %.0f TFLOP/s; hipBLASLt addmm median %.1f us"
         % (pct(dms, .5) * 1e3, w.dense_flops() / (dense_avg * 1e-3) / 1e12, pct(bms, .5) * 1e3))
+    if back:
+        log("backward: dX %.1f us (dense %.1f us), dW %.1f us (hipBLASLt full G^T X %.1f us), "
+            "db %.1f us" % (back["dx_ms"] * 1e3, back["dx_dense_ms"] * 1e3, back["dw_ms"] * 1e3,
+                            back["dw_hipblaslt_dense_ms"] * 1e3, back["db_ms"] * 1e3))
     if fms:
         log("flushed caches: bsr_linear median %.1f us, dense_linear median %.1f us (speedup %.2fx)"
             % (pct(fms, .5) * 1e3, pct(fdms, .5) * 1e3, pct(fdms, .5) / pct(fms, .5)))
@@ -405,6 +447,7 @@ def main():
             "dense_ms_median": round(pct(fdms, .5), 5),
             "speedup_vs_dense": round(pct(fdms, .5) / pct(fms, .5), 3),
             "note": "each launch after a 1 GiB device write (L2 and MALL evicted)"},
+        "backward": back,
         "pack_ms": round(pack_ms, 3),
         "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,

@@ -71,6 +71,8 @@ template <int DT> __device__ inline void store_elem(char* base, int64_t idx, flo
 
 // ---------------------------------------------------------------- bias gradient
 
+typedef uint32_t v4u __attribute__((ext_vector_type(4)));
+
 // part[chunk][n] = sum over the chunk's token rows (ascending) of G[m][n], in
 // float32.  Thread: 16 bytes of columns; grid (column blocks, chunks).
 template <int DT>
@@ -88,7 +90,22 @@ __global__ __launch_bounds__(256) void k_bias_partial(const char* __restrict__ G
     for (int i = 0; i < V; ++i)
         acc[i] = 0.0f;
     const bool full = n0 + V <= N;
-    for (int64_t m = m0; m < m1; ++m) {
+    int64_t m = m0;
+    if (full) {
+        // 8 rows' loads in flight, then their sums in row order
+        for (; m + 8 <= m1; m += 8) {
+            v4u v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+                v[u] = __builtin_nontemporal_load((const v4u*)(G + ((m + u) * ldg + n0) * ES));
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+#pragma unroll
+                for (int i = 0; i < V; ++i)
+                    acc[i] += load_elem<DT>((const char*)&v[u], i);
+        }
+    }
+    for (; m < m1; ++m) {
         if (full) {
             const uint4 v = *(const uint4*)(G + (m * ldg + n0) * ES);
 #pragma unroll
@@ -106,18 +123,28 @@ __global__ __launch_bounds__(256) void k_bias_partial(const char* __restrict__ G
             part[blockIdx.y * N + n0 + i] = acc[i];
 }
 
-// db[n] = the chunks' partial sums added in chunk order, rounded once.
+// db[n] from the chunks' partial sums in a fixed order: workgroup = 32
+// columns; lane group l (0..7) adds chunks l, l + 8, ... in order, then the 8
+// sums are added in order of l; one rounding.
 template <int DT>
 __global__ __launch_bounds__(256) void k_bias_reduce(const float* __restrict__ part, int n_chunks,
                                                      int64_t N, char* __restrict__ db)
 {
-    const int64_t n = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (n >= N)
-        return;
+    __shared__ float s_sum[8][32];
+    const int col = threadIdx.x & 31, l = threadIdx.x >> 5;
+    const int64_t n = (int64_t)blockIdx.x * 32 + col;
     float s = 0.0f;
-    for (int c = 0; c < n_chunks; ++c)
-        s += part[c * N + n];
-    store_elem<DT>(db, n, s);
+    if (n < N)
+        for (int c = l; c < n_chunks; c += 8)
+            s += part[(int64_t)c * N + n];
+    s_sum[l][col] = s;
+    __syncthreads();
+    if (l == 0 && n < N) {
+        float t = 0.0f;
+        for (int i = 0; i < 8; ++i)
+            t += s_sum[i][col];
+        store_elem<DT>(db, n, t);
+    }
 }
 
 // ---------------------------------------------------------------- weight gradient, fp32
@@ -174,10 +201,11 @@ __global__ __launch_bounds__(256) void k_gradw_plain(int32_t b_r, int32_t b_c, i
 // reads row t0 + j / 4 at column c0 + 4 (j % 4), lane i holds rows t0 .. t0 + 3
 // of column c0 + i.
 //
-// The window's kept tiles, in row-major order, are dealt to the 8 waves in
-// contiguous runs (at most 8 each, balanced to within one); a run's tiles
-// mostly share a tile row, whose G fragment is then read once per k-step.  A
-// wave reads the operands of its next tile while the current one multiplies.
+// Wave w takes one tile row of the window (its kept tiles, at most 8): the
+// row's G fragment is read once per k-step and each kept tile's X fragment
+// into registers of its own.  The rows are paired on the SIMDs by kept count
+// (largest with smallest), so every SIMD carries about the same number of
+// products.
 // Partials go to ws[chunk][tile row][tile col][1024] in accumulator order
 // (lane-major float4 runs); k_gradw_reduce adds the chunks in order.
 constexpr int GW_NT = 512;
@@ -189,6 +217,7 @@ struct GradWDims {
     int32_t n_tile_rows, n_tile_cols, n_groups, n_wcols;
     int64_t chunk_rows;
     int32_t n_chunks;
+    int32_t per_xcd;  // items per XCD (the grid is 8 per_xcd workgroups)
 };
 
 __device__ inline int gw_swz(int row) { return (row & 3) | ((row >> 1) & 4); }
@@ -233,10 +262,15 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // Items (chunk, window), chunk-major with groups fastest, are dealt to
+    // XCDs in contiguous runs (workgroup b runs on XCD b % 8): the items that
+    // share a chunk's rows of G and X then mostly share one L2.
     const int n_win = d.n_groups * d.n_wcols;
-    const int g = (int)(blockIdx.x % d.n_groups);
-    const int wc = (int)((blockIdx.x / d.n_groups) % d.n_wcols);
-    const int chunk = (int)(blockIdx.x / n_win);
+    const int item = (int)(blockIdx.x & 7) * d.per_xcd + (int)(blockIdx.x >> 3);
+    if (item >= n_win * d.n_chunks)
+        return;
+    const int chunk = item / n_win, win = item - chunk * n_win;
+    const int g = win % d.n_groups, wc = win / d.n_groups;
     const int64_t m_begin = (int64_t)chunk * d.chunk_rows;
     const int64_t m_end = min(d.M, m_begin + d.chunk_rows);
 
@@ -271,20 +305,29 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
     const int n_kept = __popcll(wmask);
     if (n_kept == 0 || m_begin >= m_end)
         return;  // uniform for the whole workgroup
-    // this wave's run of tiles
-    const int lo = wave * n_kept / 8, n_w = (wave + 1) * n_kept / 8 - lo;
-    uint64_t rest = wmask;
-    for (int i = 0; i < lo; ++i)
-        rest &= rest - 1;
-    int tj[8], tc[8];
+    // This wave's tile row: rows ranked by kept count (descending, ties by
+    // index); SIMD k (waves k and k + 4) takes the rows of rank k and 7 - k,
+    // which balances the matrix-core work of the SIMDs.
+    const int my_rank = wave < 4 ? wave : 11 - wave;
+    int tj = 0;
+    for (int j = 0; j < 8; ++j) {
+        const int cj = __popc((uint32_t)(wmask >> (8 * j)) & 0xffu);
+        int rank = 0;
+        for (int i = 0; i < 8; ++i) {
+            const int ci = __popc((uint32_t)(wmask >> (8 * i)) & 0xffu);
+            rank += (ci > cj) || (ci == cj && i < j);
+        }
+        if (rank == my_rank)
+            tj = j;
+    }
+    const uint32_t rowbits = (uint32_t)(wmask >> (8 * tj)) & 0xffu;
+    const int n_w = __popc(rowbits);
+    int tc[8];  // the row's kept tile columns, ascending
+    {
+        uint32_t rest = rowbits;
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        tj[t] = 0;
-        tc[t] = 0;
-        if (t < n_w) {
-            const int p = __builtin_ctzll(rest);
-            tj[t] = p >> 3;
-            tc[t] = p & 7;
+        for (int t = 0; t < 8; ++t) {
+            tc[t] = rest ? __builtin_ctz(rest) : 0;
             rest &= rest - 1;
         }
     }
@@ -363,23 +406,18 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
         const uint32_t stage = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE;
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
-            // the operands of tile t + 1 are read while tile t multiplies
-            F a = frag(stage, ks, tj[0]);
-            F b = frag(stage + 16384, ks, tc[0]);
+            // one G fragment for the row, one X fragment per kept tile, each
+            // in registers of its own; then the products
+            const F a = frag(stage, ks, tj);
+            F b[8];
 #pragma unroll
-            for (int t = 0; t < 8; ++t) {
-                if (t < n_w) {
-                    F an = a, bn = b;
-                    if (t + 1 < n_w) {
-                        if (tj[t + 1] != tj[t])
-                            an = frag(stage, ks, tj[t + 1]);
-                        bn = frag(stage + 16384, ks, tc[t + 1]);
-                    }
-                    acc[t] = E::mma(a, b, acc[t]);
-                    a = an;
-                    b = bn;
-                }
-            }
+            for (int t = 0; t < 8; ++t)
+                if (t < n_w)
+                    b[t] = frag(stage + 16384, ks, tc[t]);
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+                if (t < n_w)
+                    acc[t] = E::mma(a, b[t], acc[t]);
         }
     }
 
@@ -387,7 +425,7 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
 #pragma unroll
     for (int t = 0; t < 8; ++t) {
         if (t < n_w) {
-            const int64_t tile = (int64_t)(8 * g + tj[t]) * d.n_tile_cols + (8 * wc + tc[t]);
+            const int64_t tile = (int64_t)(8 * g + tj) * d.n_tile_cols + (8 * wc + tc[t]);
             float* dst = ws + ((int64_t)chunk * d.n_tile_rows * d.n_tile_cols + tile) * 1024;
 #pragma unroll
             for (int qq = 0; qq < 4; ++qq) {
@@ -457,7 +495,8 @@ hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, in
 {
     const int V = dtype == LPV_F32 ? 4 : 8;
     const int64_t bx = (N + 256 * V - 1) / (256 * V);
-    int64_t n_chunks = (2048 + bx - 1) / bx;
+    // about 1024 workgroups of 8 waves, at least 64 rows each
+    int64_t n_chunks = (1024 + bx - 1) / bx;
     n_chunks = max((int64_t)1, min(n_chunks, (M + 63) / 64));
     const int64_t rows = (M + n_chunks - 1) / n_chunks;
     n_chunks = M > 0 ? (M + rows - 1) / rows : 1;
@@ -481,7 +520,7 @@ hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, in
     }
     e = hipGetLastError();
     if (e == hipSuccess) {
-        const dim3 grid((unsigned)((N + 255) / 256));
+        const dim3 grid((unsigned)((N + 31) / 32));
         if (dtype == LPV_BF16)
             hipLaunchKernelGGL(k_bias_reduce<LPV_BF16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
         else if (dtype == LPV_F16)
@@ -531,7 +570,8 @@ hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
     hipError_t e = hipMallocAsync((void**)&ws, (size_t)(d.n_chunks * chunk_stride) * sizeof(float), s);
     if (e != hipSuccess)
         return e;
-    const dim3 grid((unsigned)(n_win * d.n_chunks)), block(GW_NT);
+    d.per_xcd = (int32_t)((n_win * d.n_chunks + 7) / 8);
+    const dim3 grid((unsigned)(8 * d.per_xcd)), block(GW_NT);
     const dim3 rgrid((unsigned)((total + 255) / 256));
     if (h->dtype == LPV_BF16) {
         hipLaunchKernelGGL(k_gradw_tiles<LPV_BF16>, grid, block, 0, s, d, (const int32_t*)h->step_ptr,
