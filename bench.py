@@ -119,6 +119,12 @@ def kernel_label(name):
     for key in ("k_pack_plan", "k_pack_compact", "k_sched_fill", "k_stream_fill", "k_walk_fill"):
         if key in name:
             return key + " (lpv_bsr_pack)"
+    for key, api in (("k_gradw_tiles", "lpv_bsr_grad_w"), ("k_gradw_reduce", "lpv_bsr_grad_w"),
+                     ("k_gradw_plain", "lpv_bsr_grad_w"), ("k_bias_partial", "lpv_bias_grad"),
+                     ("k_bias_reduce", "lpv_bias_grad"), ("k_transpose_blocks", "lpv_bsr_transpose"),
+                     ("k_unpack", "lpv_bsr_unpack")):
+        if key in name:
+            return "%s (%s)" % (key, api)
     return name.split("(")[0][:72]
 
 
@@ -128,7 +134,7 @@ def write_stats(stats_csv, command):
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
     text = ["# rocprofv3 kernel statistics: DeiT-B fc1 (X 50432 x 768 -> 3072), bf16, 32x32 blocks, "
-            "50% block sparsity", "",
+            "50% block sparsity, forward and backward", "",
             "Profiled run, then this summary (from the repository root on one MI355X):", "", "```",
             "rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
             "-- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed", command, "```", "",
@@ -145,7 +151,11 @@ def write_stats(stats_csv, command):
                  "dense path.  Kept work of one block-sparse launch: 118.98 GFLOP, so the "
                  "block-sparse average above is %.0f TFLOP/s (%.1f%% of the 2.5 PFLOP/s bf16 "
                  "matrix-core peak); `bench.py` times the same launches with HIP events on their "
-                 "stream and reports that average as `roofline.achieved`."
+                 "stream and reports that average as `roofline.achieved`.  The backward rows: "
+                 "dX is the block-sparse forward kernel on the transposed handle (its calls "
+                 "are counted with the forward's), dW is k_gradw_tiles + k_gradw_reduce, db is "
+                 "k_bias_partial + k_bias_reduce; the second hipBLASLt kernel (Cijk_Ailk) is "
+                 "the dense G^T X reference."
                  % (118.98e9 / (avg_us * 1e-6) / 1e12, 118.98e9 / (avg_us * 1e-6) / 1e12 / 25.0)]
     with open(STATS_FILE, "w") as f:
         f.write("\n".join(text) + "\n")
