@@ -59,6 +59,9 @@ class Oracle:
         lib.lpvo_grad_w.restype = i64
         lib.lpvo_grad_bias.argtypes = [i32, vp, i64, i64, i64, vp]
         lib.lpvo_grad_bias.restype = i32
+        lib.lpvo_delta_curve.argtypes = [i32, vp, i64, i64, i64, i32, i32, vp, vp, i64,
+                                         ctypes.c_double, vp, i32, vp]
+        lib.lpvo_delta_curve.restype = i32
         self.lib = lib
         self.path = path
 
@@ -201,6 +204,28 @@ class Oracle:
             raise ValueError("lpvo_grad_bias rejected its arguments")
         return db
 
+    def delta_curve(self, W, dtype, b_r, b_c, grad, samples, kappa, pcts):
+        """The delta curve: float64 delta at each sparsity percentage in
+        ``pcts`` (grad: N x K, samples: n x N x K per-sample gradients)."""
+        W = np.ascontiguousarray(W)
+        grad = np.ascontiguousarray(grad)
+        samples = np.ascontiguousarray(samples)
+        for a, nm in ((W, "W"), (grad, "grad"), (samples, "samples")):
+            _check(a, dtype, nm)
+        N, K = W.shape
+        if grad.shape != (N, K) or samples.ndim != 3 or samples.shape[1:] != (N, K):
+            raise ValueError("grad must be N x K and samples n x N x K")
+        if b_r <= 0 or b_c <= 0 or N % b_r or K % b_c:
+            raise ValueError("block %dx%d does not divide weight %dx%d" % (b_r, b_c, N, K))
+        pcts = np.ascontiguousarray(pcts, dtype=np.int32)
+        out = np.empty(len(pcts), np.float64)
+        rc = self.lib.lpvo_delta_curve(_CODES[dtype], _ptr(W), K, N, K, b_r, b_c, _ptr(grad),
+                                       _ptr(samples), samples.shape[0], float(kappa), _ptr(pcts),
+                                       len(pcts), _ptr(out))
+        if rc:
+            raise ValueError("lpvo_delta_curve failed (%d)" % rc)
+        return out
+
     def block_scores(self, W, dtype, b_r, b_c, G=None):
         """Block scores, float64 R x C: the mean of |W * G| per block (the
         paper's average-pooled Taylor score, Sec. 3.1), or without G the sum of
@@ -308,6 +333,10 @@ def grad_w(G, X, dtype, b_r, b_c, mask):
 
 def grad_bias(G, dtype):
     return default().grad_bias(G, dtype)
+
+
+def delta_curve(W, dtype, b_r, b_c, grad, samples, kappa, pcts):
+    return default().delta_curve(W, dtype, b_r, b_c, grad, samples, kappa, pcts)
 
 
 def block_scores(W, dtype, b_r, b_c, G=None):

@@ -553,3 +553,77 @@ int lpvo_grad_bias(int dtype, const void* G, int64_t ldg, int64_t M, int64_t N, 
     }
     return 0;
 }
+
+/* ------------------------------------------------------------------------ */
+/* The delta curve of a layer (Sec. 3.3, the empirical-Fisher Hessian)       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The paper collects, per layer, the second-order Taylor term of the output
+ * distortion against the pruning ratio alpha:
+ *   delta(alpha) = grad^T dW(alpha) + 1/2 dW(alpha)^T H dW(alpha),
+ * with the Hessian approximated by the empirical Fisher over N calibration
+ * samples, H = kappa I + (1/N) sum_n g_n g_n^T (g_n: the per-sample gradient of
+ * the layer's weight, flattened).  dW(alpha) is the weight change of pruning at
+ * ratio alpha: -W[e] for every element e of a dropped block, 0 elsewhere.  The
+ * blocks dropped at a sparsity percentage p (alpha = p / 100) are those outside
+ * the top ceil((100 - p) R C / 100) by the Sec. 3.1 score with the gradient
+ * (mean |W grad| per block; ties to the lower index), exactly as
+ * lpvo_block_scores + lpvo_keep_count + lpvo_mask_topk give them.
+ *
+ * This function is the direct definition at every requested percentage:
+ *   delta = sum_e grad[e] dW[e]
+ *         + 1/2 ( kappa sum_e dW[e]^2 + (1/N) sum_n (sum_e g_n[e] dW[e])^2 ),
+ * each sum over e in row-major order, n ascending, in float64.
+ */
+int lpvo_delta_curve(int dtype, const void* W, int64_t ldw, int64_t N, int64_t K, int b_r, int b_c,
+                     const void* grad, const void* samples, int64_t n_samples, double kappa,
+                     const int32_t* pcts, int n_points, double* delta)
+{
+    if (!lpvo_elem_size(dtype) || !grid_ok(N, K, b_r, b_c) || ldw < K || !W || !grad ||
+        n_samples < 0 || (n_samples > 0 && !samples) || n_points < 0 || (n_points > 0 && (!pcts || !delta)))
+        return -1;
+    for (int i = 0; i < n_points; ++i)
+        if (pcts[i] < 0 || pcts[i] > 100)
+            return -1;
+    const int64_t R = N / b_r, C = K / b_c, nb = R * C, D = N * K;
+    double* scores = (double*)malloc(sizeof(double) * (size_t)(nb + 1));
+    uint8_t* mask = (uint8_t*)malloc((size_t)nb + 1);
+    double* dw = (double*)malloc(sizeof(double) * (size_t)(D + 1));
+    int rc = 0;
+    if (!scores || !mask || !dw) {
+        rc = -2;
+        goto out;
+    }
+    /* the gradient is N x K with row stride K (grad) */
+    if (lpvo_block_scores(dtype, W, ldw, grad, K, N, K, b_r, b_c, scores)) {
+        rc = -1;
+        goto out;
+    }
+    for (int i = 0; i < n_points; ++i) {
+        const int64_t keep = lpvo_keep_count(nb, pcts[i]);
+        rc = lpvo_mask_topk(scores, nb, keep, mask);
+        if (rc)
+            goto out;
+        for (int64_t n = 0; n < N; ++n)
+            for (int64_t k = 0; k < K; ++k)
+                dw[n * K + k] = mask[(n / b_r) * C + (k / b_c)] ? 0.0 : -dec_one(dtype, W, n * ldw + k);
+        double lin = 0.0, sq = 0.0, fisher = 0.0;
+        for (int64_t e = 0; e < D; ++e) {
+            lin += dec_one(dtype, grad, e) * dw[e];
+            sq += dw[e] * dw[e];
+        }
+        for (int64_t s = 0; s < n_samples; ++s) {
+            double p = 0.0;
+            for (int64_t e = 0; e < D; ++e)
+                p += dec_one(dtype, samples, s * D + e) * dw[e];
+            fisher += p * p;
+        }
+        delta[i] = lin + 0.5 * (kappa * sq + (n_samples > 0 ? fisher / (double)n_samples : 0.0));
+    }
+out:
+    free(scores);
+    free(mask);
+    free(dw);
+    return rc;
+}

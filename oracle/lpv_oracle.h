@@ -78,6 +78,17 @@ int64_t lpvo_grad_w(int dtype, const void* G, int64_t ldg, const void* X, int64_
                     int64_t N, int64_t K, int b_r, int b_c, const uint8_t* mask, double* dW);
 int lpvo_grad_bias(int dtype, const void* G, int64_t ldg, int64_t M, int64_t N, double* db);
 
+/* The delta curve (second-order Taylor term of pruning against the pruning
+ * ratio, empirical-Fisher Hessian kappa I + (1/n) sum g g^T) at each sparsity
+ * percentage pcts[i] (0..100): delta[i] = grad . dW + 1/2 (kappa |dW|^2 +
+ * (1/n) sum_s (g_s . dW)^2), dW = -W on the blocks dropped at that percentage
+ * by the gradient's Taylor score.  grad: N x K (row stride K); samples:
+ * n_samples x N x K, contiguous.  Returns 0, -1 on a bad argument, -2 when
+ * host memory runs out. */
+int lpvo_delta_curve(int dtype, const void* W, int64_t ldw, int64_t N, int64_t K, int b_r, int b_c,
+                     const void* grad, const void* samples, int64_t n_samples, double kappa,
+                     const int32_t* pcts, int n_points, double* delta);
+
 #ifdef __cplusplus
 }
 #endif

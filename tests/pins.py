@@ -494,4 +494,74 @@ def pin_grad_exact_integers(orc):
     assert k == dW.shape[0]
 
 
+# ---------------------------------------------------------------- delta curve
+
+def _delta_case(seed, N, K, n_s, dtype="f32", integers=False):
+    g = np.random.default_rng(seed)
+    if integers:
+        draw = lambda shape: g.integers(-3, 4, shape).astype(np.float32)
+    else:
+        draw = lambda shape: g.normal(0, 1, shape).astype(np.float32)
+    return (wl.quantize(draw((N, K)), dtype), wl.quantize(draw((N, K)), dtype),
+            wl.quantize(draw((n_s, N, K)), dtype))
+
+
+def _dropped_numpy(W, grad, b_r, b_c, p):
+    """Dropped-block mask with numpy alone: block means of |W grad|, ranked by
+    (-score, row-major index), the top ceil((100 - p) R C / 100) kept."""
+    N, K = W.shape
+    R, C = N // b_r, K // b_c
+    a = np.abs(W.astype(np.float64) * grad.astype(np.float64))
+    sc = a.reshape(R, b_r, C, b_c).sum(axis=(1, 3)).ravel() / (b_r * b_c)
+    keep = -((p - 100) * R * C // 100)  # integer ceiling of (100 - p) R C / 100
+    order = np.lexsort((np.arange(R * C), -sc))
+    kept = np.zeros(R * C, bool)
+    kept[order[:keep]] = True
+    return ~_expand(kept.reshape(R, C).astype(np.uint8), b_r, b_c)
+
+
+def pin_delta_zero_without_pruning(orc):
+    W, gr, S = _delta_case(81, 64, 32, 3)
+    assert orc.delta_curve(W, "f32", 16, 16, gr, S, 0.5, [0])[0] == 0.0
+
+
+def pin_delta_vs_dense_fisher(orc):
+    # the explicit Hessian kappa I + (1/n) sum g g^T as a dense numpy matrix,
+    # the dropped set from numpy's own block scores and lexsort
+    for (b_r, b_c, integers) in [(16, 16, False), (16, 32, False), (32, 16, True)]:
+        W, gr, S = _delta_case(82 + b_c, 64, 64, 4, integers=integers)
+        pcts = [0, 10, 25, 50, 75, 90, 100]
+        got = orc.delta_curve(W, "f32", b_r, b_c, gr, S, 0.25, pcts)
+        Gs = S.reshape(4, -1).astype(np.float64)
+        H = 0.25 * np.eye(Gs.shape[1]) + Gs.T @ Gs / 4
+        for i, p in enumerate(pcts):
+            dw = np.where(_dropped_numpy(W, gr, b_r, b_c, p), -W.astype(np.float64), 0.0).ravel()
+            ref = gr.astype(np.float64).ravel() @ dw + 0.5 * dw @ H @ dw
+            if integers:
+                assert got[i] == ref, (p, got[i], ref)  # every term exact
+            else:
+                assert abs(got[i] - ref) <= 1e-10 * max(1.0, abs(ref)), (p, got[i], ref)
+
+
+def pin_delta_incremental_update(orc):
+    # the paper's update from one ratio to the next: with d the newly pruned
+    # part and D the previous change, delta_k - delta_{k-1} =
+    # grad' . d + (d / 2 + D)^T H' d, H' the Fisher restricted to d's support
+    W, gr, S = _delta_case(85, 64, 96, 5)
+    pcts = [0, 20, 40, 60, 80, 100]
+    got = orc.delta_curve(W, "f32", 16, 32, gr, S, 0.1, pcts)
+    Gs = S.reshape(5, -1).astype(np.float64)
+    prev = np.zeros(W.size)
+    acc = 0.0
+    for i, p in enumerate(pcts):
+        cur = np.where(_dropped_numpy(W, gr, 16, 32, p), -W.astype(np.float64), 0.0).ravel()
+        d = cur - prev
+        sup = d != 0
+        # H' d: the columns of H on d's support (a D-vector)
+        Hd = 0.1 * d + Gs.T @ (Gs[:, sup] @ d[sup]) / 5
+        acc += gr.astype(np.float64).ravel()[sup] @ d[sup] + (0.5 * d + prev) @ Hd
+        assert abs(got[i] - acc) <= 1e-9 * max(1.0, abs(acc)), (p, got[i], acc)
+        prev = cur
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -71,6 +71,15 @@ MUTANTS = {
                        "x[j] = dec_one(dtype, G, m * ldg + c * b_c + j);"),
     "gradb_first_row_dropped": ("for (int64_t m = 0; m < M; ++m)\n            s += dec_one(dtype, G, m * ldg + n);",
                                 "for (int64_t m = 1; m < M; ++m)\n            s += dec_one(dtype, G, m * ldg + n);"),
+    "delta_half_dropped": ("delta[i] = lin + 0.5 * (kappa * sq", "delta[i] = lin + (kappa * sq"),
+    "delta_change_sign": (": -dec_one(dtype, W, n * ldw + k);", ": dec_one(dtype, W, n * ldw + k);"),
+    "delta_kept_blocks": ("? 0.0 : -dec_one(dtype, W, n * ldw + k);",
+                          "? -dec_one(dtype, W, n * ldw + k) : 0.0;"),
+    "delta_kappa_dropped": ("0.5 * (kappa * sq +", "0.5 * (0.0 * sq +"),
+    "delta_fisher_not_averaged": ("fisher / (double)n_samples", "fisher"),
+    "delta_linear_term_dropped": ("lin += dec_one(dtype, grad, e) * dw[e];", "lin += 0.0;"),
+    "delta_l2_ranking": ("lpvo_block_scores(dtype, W, ldw, grad, K, N, K, b_r, b_c, scores)",
+                         "lpvo_block_scores(dtype, W, ldw, NULL, K, N, K, b_r, b_c, scores)"),
     "topk_keeps_lowest": ("    if (si > sj)\n        return -1;\n    if (si < sj)\n        return 1;",
                           "    if (si > sj)\n        return 1;\n    if (si < sj)\n        return -1;"),
 }
