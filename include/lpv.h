@@ -254,6 +254,37 @@ lpv_status lpv_bsr_grad_w(const lpv_bsr* h, const void* G, int64_t ldg, const vo
 lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
                          void* db, void* stream);
 
+/*
+ * lpv_delta_curve -- the delta curve of one layer (Sec. 3.3): the second-order
+ * Taylor term of pruning it at ratio alpha,
+ *   delta(alpha) = grad . dW + 1/2 dW^T H dW,  H = kappa I + (1/n) sum_s g_s g_s^T
+ * (the empirical Fisher over n calibration samples), at each sparsity
+ * percentage pcts[i] (alpha = pcts[i] / 100).  dW = -W on the blocks dropped at
+ * that percentage: those outside the top ceil((100 - p) R C / 100) by the
+ * Taylor score mean |W grad| per block (lpv_mask_topk's ranking with G = grad;
+ * ties to the lower row-major index), so the dropped sets are nested.
+ *
+ * W        device, N x K (row stride ldw), element type dt.
+ * grad     device, N x K (row stride ldg), dt: the layer's loss gradient.
+ * samples  device, n_samples per-sample gradients, each N x K with row stride
+ *          lds, sample s at samples + s * sample_stride elements; dt.
+ * pcts     host, n_points (1..128) sparsity percentages, non-decreasing in
+ *          [0, 100].
+ * delta    device, n_points float64, receives the curve.
+ *
+ * The curve is built with the paper's incremental update over the ratio
+ * steps: float64 dot products of every per-sample gradient (and of grad, and W)
+ * with -W over every block, then the steps in rank order.  All sums run in a
+ * fixed order.  At most 2^17 blocks, n_samples <= 65000.  Allocates and frees a
+ * stream-ordered workspace; no host synchronisation.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, BLOCK, ALLOC, HIP.
+ */
+lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                           int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
+                           const void* samples, int64_t lds, int64_t sample_stride,
+                           int64_t n_samples, double kappa, const int32_t* pcts, int32_t n_points,
+                           double* delta, void* stream);
+
 /* Release a handle and its device buffers.  NULL-safe.  The caller must make
  * sure no enqueued work still uses it. */
 void lpv_bsr_destroy(lpv_bsr* h);

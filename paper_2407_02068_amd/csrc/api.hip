@@ -542,6 +542,76 @@ lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_d
     return e == hipSuccess ? LPV_OK : hip_fail(e, "bias_grad launch");
 }
 
+lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                           int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
+                           const void* samples, int64_t lds, int64_t sample_stride,
+                           int64_t n_samples, double kappa, const int32_t* pcts, int32_t n_points,
+                           double* delta, void* stream)
+{
+    g_err[0] = 0;
+    const int es = elem_size(dt);
+    if (!es)
+        return fail(LPV_ERR_DTYPE, "unknown element type %d", (int)dt);
+    if (check_block(b_r) || check_block(b_c))
+        return fail(LPV_ERR_BLOCK, "block %dx%d: each side must be 16, 32 or 64", b_r, b_c);
+    if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM)
+        return fail(LPV_ERR_SHAPE, "weight %lldx%lld: each side must be in [1, %lld]",
+                    (long long)N, (long long)K, (long long)MAX_DIM);
+    if (N % b_r || K % b_c)
+        return fail(LPV_ERR_SHAPE, "block %dx%d does not divide weight %lldx%lld", b_r, b_c,
+                    (long long)N, (long long)K);
+    if ((N / b_r) * (K / b_c) > lpv::DELTA_MAX_BLOCKS)
+        return fail(LPV_ERR_SHAPE, "%lld blocks: at most %lld are supported",
+                    (long long)((N / b_r) * (K / b_c)), (long long)lpv::DELTA_MAX_BLOCKS);
+    if (n_samples < 0 || n_samples > 65000)  // one grid row per vector
+        return fail(LPV_ERR_SHAPE, "n_samples = %lld is out of range [0, 65000]",
+                    (long long)n_samples);
+    if (n_points < 1 || n_points > lpv::DELTA_MAX_POINTS || !pcts)
+        return fail(LPV_ERR_INVALID_ARG, "1 to %d sparsity points are needed",
+                    lpv::DELTA_MAX_POINTS);
+    for (int i = 0; i < n_points; ++i)
+        if (pcts[i] < 0 || pcts[i] > 100 || (i > 0 && pcts[i] < pcts[i - 1]))
+            return fail(LPV_ERR_INVALID_ARG, "sparsity points must ascend within [0, 100]");
+    if (!(kappa == kappa) || kappa > 1e300 || kappa < -1e300)
+        return fail(LPV_ERR_INVALID_ARG, "kappa must be finite");
+    if (!W || !grad || !delta || (n_samples > 0 && !samples))
+        return fail(LPV_ERR_INVALID_ARG, "W, grad, delta (and samples) must not be NULL");
+    if (!aligned16(W) || !aligned16(grad) || (n_samples > 0 && !aligned16(samples)) ||
+        (uintptr_t)delta % 8)
+        return fail(LPV_ERR_INVALID_ARG, "W, grad and samples must be 16-byte aligned, delta 8");
+    if (ldw < K || ldg < K || (n_samples > 0 && lds < K) || ldw > MAX_LD || ldg > MAX_LD ||
+        lds > MAX_LD || (ldw * es) % 16 || (ldg * es) % 16 || (n_samples > 0 && (lds * es) % 16))
+        return fail(LPV_ERR_INVALID_ARG, "ldw, ldg, lds must be in [K, 2^22] and multiples of 16 "
+                                         "bytes");
+    if (n_samples > 0 && (sample_stride < (N - 1) * lds + K || (sample_stride * es) % 16))
+        return fail(LPV_ERR_INVALID_ARG, "sample_stride must cover one sample and be a multiple "
+                                         "of 16 bytes");
+    lpv::DeltaCall c = {};
+    c.W = W;
+    c.ldw = ldw;
+    c.N = N;
+    c.K = K;
+    c.dtype = dt;
+    c.b_r = b_r;
+    c.b_c = b_c;
+    c.grad = grad;
+    c.ldg = ldg;
+    c.samples = samples;
+    c.lds = lds;
+    c.stride = sample_stride;
+    c.n_samples = n_samples;
+    c.kappa = kappa;
+    c.n_points = n_points;
+    const int64_t nb = (N / b_r) * (K / b_c);
+    for (int i = 0; i < n_points; ++i)
+        c.keep[i] = (int32_t)(((100 - (int64_t)pcts[i]) * nb + 99) / 100);
+    c.delta = delta;
+    hipError_t e = lpv::launch_delta_curve(c, (hipStream_t)stream);
+    if (e == hipErrorOutOfMemory)
+        return fail(LPV_ERR_ALLOC, "workspace allocation failed");
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "delta_curve launch");
+}
+
 void lpv_bsr_destroy(lpv_bsr* h)
 {
     free_handle(h);

@@ -94,6 +94,26 @@ struct MaskCall {
     double* scores;
 };
 hipError_t launch_mask_topk(const MaskCall& m, hipStream_t s);
+hipError_t launch_block_scores(const MaskCall& m, hipStream_t s);  // scores only
+
+// delta.hip
+constexpr int DELTA_MAX_POINTS = 128;
+constexpr int64_t DELTA_MAX_BLOCKS = (int64_t)1 << 17;
+struct DeltaCall {
+    const void* W;  // N x K, row stride ldw
+    int64_t ldw, N, K;
+    int dtype;
+    int32_t b_r, b_c;
+    const void* grad;  // N x K, row stride ldg
+    int64_t ldg;
+    const void* samples;  // n_samples x (N x K, row stride lds), sample stride `stride`
+    int64_t lds, stride, n_samples;
+    double kappa;
+    int32_t n_points;
+    int32_t keep[DELTA_MAX_POINTS];  // kept blocks at each point, non-increasing
+    double* delta;                   // n_points, device
+};
+hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s);
 
 // backward.hip
 struct GradWCall {

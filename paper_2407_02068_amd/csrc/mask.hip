@@ -132,7 +132,7 @@ __global__ __launch_bounds__(SEL_THREADS) void k_mask_topk(const double* __restr
 
 }  // namespace
 
-hipError_t launch_mask_topk(const MaskCall& m, hipStream_t s)
+hipError_t launch_block_scores(const MaskCall& m, hipStream_t s)
 {
     const int64_t R = m.N / m.b_r, C = m.K / m.b_c, nb = R * C;
     if (nb > 0) {
@@ -155,10 +155,16 @@ hipError_t launch_mask_topk(const MaskCall& m, hipStream_t s)
             LPV_SCORES_DT(LPV_F32);
 #undef LPV_SCORES_DT
 #undef LPV_SCORES
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess)
-            return e;
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_mask_topk(const MaskCall& m, hipStream_t s)
+{
+    const int64_t nb = (m.N / m.b_r) * (m.K / m.b_c);
+    const hipError_t e = launch_block_scores(m, s);
+    if (e != hipSuccess)
+        return e;
     hipLaunchKernelGGL(k_mask_topk, dim3(1), dim3(SEL_THREADS), 0, s, (const double*)m.scores, nb,
                        m.n_keep, m.mask);
     return hipGetLastError();

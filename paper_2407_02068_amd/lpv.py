@@ -21,7 +21,7 @@ DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 EPI = {None: 0, "none": 0, "gelu": 1}
 EXPORTED = ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
             "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
-            "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad",
+            "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_delta_curve",
             "lpv_bsr_destroy", "lpv_status_str", "lpv_last_error")
 
 
@@ -67,9 +67,11 @@ def lib():
     L.lpv_bsr_transpose.argtypes = [vp, vp, ctypes.POINTER(vp)]
     L.lpv_bsr_grad_w.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.lpv_bias_grad.argtypes = [vp, i64, i64, i64, i32, vp, vp]
+    L.lpv_delta_curve.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, vp, i64, i64, i64,
+                                  ctypes.c_double, vp, i32, vp, vp]
     for f in ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
               "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
-              "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad"):
+              "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_delta_curve"):
         getattr(L, f).restype = i32
     L.lpv_bsr_destroy.argtypes = [vp]
     L.lpv_bsr_destroy.restype = None
@@ -322,4 +324,30 @@ def bias_grad(G, out=None, stream=None):
         raise ValueError("out must be a contiguous %s tensor of %d elements" % (G.dtype, N))
     _check(lib().lpv_bias_grad(gp, ldg, M, N, DTYPES[G.dtype], ctypes.c_void_p(out.data_ptr()),
                                _stream(stream)), "lpv_bias_grad")
+    return out
+
+
+def delta_curve(W, grad, samples, b_r, b_c, kappa, pcts, out=None, stream=None):
+    """lpv_delta_curve: the layer's delta curve at the sparsity percentages
+    ``pcts`` (non-decreasing).  W, grad: N x K; samples: n x N x K per-sample
+    gradients (same dtype).  Returns a float64 device tensor of len(pcts)."""
+    if grad.dtype != W.dtype or samples.dtype != W.dtype:
+        raise TypeError("W, grad and samples must share a dtype")
+    if samples.dim() != 3 or tuple(samples.shape[1:]) != tuple(W.shape) or grad.shape != W.shape:
+        raise ValueError("grad must be N x K and samples n x N x K")
+    N, K = W.shape
+    n = samples.shape[0]
+    if n > 0 and (samples.stride(2) != 1 or (N > 1 and samples.stride(1) < K)):
+        raise ValueError("samples must have unit stride along K")
+    pc = (ctypes.c_int32 * len(pcts))(*[int(p) for p in pcts])
+    if out is None:
+        out = torch.empty(len(pcts), dtype=torch.float64, device=W.device)
+    wp, ldw = _mat(W, "W")
+    gp, ldg = _mat(grad, "grad")
+    lds = samples.stride(1) if n > 0 else K
+    stride = samples.stride(0) if n > 0 else N * K
+    _check(lib().lpv_delta_curve(wp, ldw, N, K, DTYPES[W.dtype], b_r, b_c, gp, ldg,
+                                 ctypes.c_void_p(samples.data_ptr()), lds, stride, n, float(kappa),
+                                 pc, len(pcts), ctypes.c_void_p(out.data_ptr()), _stream(stream)),
+           "lpv_delta_curve")
     return out

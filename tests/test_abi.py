@@ -160,3 +160,25 @@ def test_backward_rejects_bad_arguments(L):
     assert bg(db=0) == INVALID and bg(db=FAKE + 1) == INVALID
     assert bg(G=0) == INVALID and bg(G=FAKE + 8) == INVALID
     assert L.lpv_last_error().decode() != ""
+
+
+def test_delta_curve_rejects_bad_arguments(L):
+    pc = (ctypes.c_int32 * 3)(0, 50, 100)
+    bad = (ctypes.c_int32 * 3)(0, 60, 50)
+
+    def dc(W=FAKE, ldw=768, N=3072, K=768, dt=2, b_r=32, b_c=32, grad=FAKE + (1 << 32), ldg=768,
+           S=FAKE + (2 << 32), lds=768, stride=3072 * 768, n=4, kappa=0.1, pcts=pc, npt=3,
+           out=FAKE + (3 << 32)):
+        return L.lpv_delta_curve(W, ldw, N, K, dt, b_r, b_c, grad, ldg, S, lds, stride, n,
+                                 ctypes.c_double(kappa), pcts, npt, out, None)
+    assert dc(dt=9) == DTYPE and dc(b_r=8) == BLOCK
+    assert dc(N=3072 + 16) == SHAPE and dc(N=1 << 17) == SHAPE and dc(n=-1) == SHAPE
+    assert dc(n=70000) == SHAPE
+    assert dc(N=16384, K=16384, b_r=16, b_c=16, ldw=16384, ldg=16384, lds=16384,
+              stride=16384 * 16384) == SHAPE  # more than 2^17 blocks
+    assert dc(pcts=bad) == INVALID and dc(npt=0) == INVALID and dc(npt=200) == INVALID
+    assert dc(pcts=None) == INVALID and dc(kappa=float("nan")) == INVALID
+    assert dc(W=0) == INVALID and dc(grad=0) == INVALID and dc(out=0) == INVALID
+    assert dc(S=0) == INVALID and dc(W=FAKE + 8) == INVALID and dc(out=FAKE + (3 << 32) + 4) == INVALID
+    assert dc(ldw=700) == INVALID and dc(lds=770) == INVALID and dc(stride=100) == INVALID
+    assert L.lpv_last_error().decode() != ""

@@ -1,0 +1,78 @@
+"""GPU parity of lpv_delta_curve against the float64 oracle, which evaluates
+the delta curve's definition directly at every ratio (the GPU takes the
+paper's incremental update; both in float64, so they agree to rounding)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads as wl
+from gpu_util import dev, say
+from paper_2407_02068_amd import lpv
+
+pytestmark = pytest.mark.gpu
+
+TOL = 1e-9  # infinity-norm relative error: float64 sums in another order
+
+
+def inputs(seed, N, K, n_s, dtype):
+    g = np.random.default_rng(seed)
+    W = wl.quantize(g.normal(0, 0.02, (N, K)).astype(np.float32), dtype)
+    grad = wl.quantize(g.normal(0, 1e-3, (N, K)).astype(np.float32), dtype)
+    S = wl.quantize(g.normal(0, 1e-2, (n_s, N, K)).astype(np.float32), dtype)
+    return W, grad, S
+
+
+def check(W, grad, S, dtype, b_r, b_c, kappa, pcts, what=""):
+    say("delta_curve", what, dtype, W.shape, (b_r, b_c), "n=%d" % S.shape[0], pcts)
+    Sd = dev(S.reshape(S.shape[0], -1), dtype).reshape(S.shape) if S.shape[0] else \
+        torch.empty((0,) + W.shape, dtype=dev(W, dtype).dtype, device="cuda")
+    got = lpv.delta_curve(dev(W, dtype), dev(grad, dtype), Sd, b_r, b_c, kappa, pcts)
+    torch.cuda.synchronize()
+    got = got.cpu().numpy()
+    ref = oracle.delta_curve(W, dtype, b_r, b_c, grad, S, kappa, pcts)
+    scale = max(np.abs(ref).max(), 1e-300)
+    err = np.abs(got - ref).max() / scale
+    say("  rel err %.2e (max |delta| %.3e)" % (err, scale))
+    assert err <= TOL
+    return got, ref
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16", "f32"])
+@pytest.mark.parametrize("b_r,b_c", [(32, 32), (16, 16), (64, 32), (16, 64)])
+def test_delta_curve_matches_oracle(dtype, b_r, b_c):
+    W, grad, S = inputs(101 + b_r + b_c, 256, 192, 5, dtype)
+    check(W, grad, S, dtype, b_r, b_c, 0.05, list(range(0, 101, 10)))
+
+
+@pytest.mark.parametrize("n_s", [0, 1, 33])
+def test_delta_curve_sample_counts(n_s):
+    W, grad, S = inputs(102, 128, 256, n_s, "bf16")
+    check(W, grad, S, "bf16", 32, 32, 0.0, [0, 5, 50, 95, 100], "samples")
+
+
+def test_delta_curve_points():
+    W, grad, S = inputs(103, 192, 128, 4, "bf16")
+    # one point, repeated points, a point at 100%, an uneven grid
+    check(W, grad, S, "bf16", 16, 16, 0.2, [100], "one point")
+    check(W, grad, S, "bf16", 16, 16, 0.2, [30, 30, 31, 99], "repeats")
+    got, _ = check(W, grad, S, "bf16", 16, 16, 0.2, [0, 0], "zeros")
+    assert np.all(got == 0.0)
+
+
+def test_delta_curve_ties_in_the_ranking():
+    # equal scores everywhere: blocks are dropped from the highest index down
+    W = np.ones((128, 128), np.float32)
+    grad = np.ones((128, 128), np.float32)
+    g = np.random.default_rng(104)
+    S = g.integers(-2, 3, (3, 128, 128)).astype(np.float32)
+    check(W, grad, S, "f32", 32, 32, 0.5, [0, 25, 50, 75, 100], "ties")
+
+
+def test_delta_curve_headline_layer():
+    # DeiT-B fc1's weight with 8 per-sample gradients at a few ratios
+    w = wl.b_fc1(with_x=False)
+    g = np.random.default_rng(105)
+    grad = wl.quantize(g.normal(0, 1e-3, w.W.shape).astype(np.float32), "bf16")
+    S = wl.quantize(g.normal(0, 1e-2, (8,) + w.W.shape).astype(np.float32), "bf16")
+    check(w.W, grad, S, "bf16", 32, 32, 1e-4, [0, 30, 50, 70], "b_fc1")
