@@ -269,6 +269,34 @@ def time_backward(w, h, W, X, steps, tt, to_dev):
                     "reduction; G seeded N(0, 1)"}
 
 
+def time_delta_curve(w, W, steps, to_dev):
+    """The delta curve of the same layer (Sec. 3.3): 64 seeded per-sample
+    gradients of the weight, the 21 sparsity points 0, 5, .., 100.  The pass
+    over the per-sample gradients bounds it: reported against HBM."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_2407_02068_amd import lpv
+    n_s = 64
+    g = wl.rng(4, 0, wl.T_GRAD)
+    grad = to_dev(wl.quantize(g.normal(0, 1e-3, (w.N, w.K)).astype(np.float32), w.dtype))
+    S = torch.empty((n_s, w.N, w.K), dtype=W.dtype, device="cuda")
+    for i in range(n_s):  # generated per sample to bound host memory
+        S[i] = to_dev(wl.quantize(g.normal(0, 1e-2, (w.N, w.K)).astype(np.float32), w.dtype))
+    pcts = list(range(0, 101, 5))
+    out = torch.empty(len(pcts), dtype=torch.float64, device="cuda")
+    _, ms = time_launches(lambda: lpv.delta_curve(W, grad, S, w.b_r, w.b_c, 1e-4, pcts, out),
+                          max(10, steps // 2), 5)
+    avg = sum(ms) / len(ms)
+    alg = (n_s + 2) * w.N * w.K * 2  # every vector (samples, grad, W) read once
+    return {"ms": round(avg, 5), "n_samples": n_s, "points": len(pcts),
+            "hbm_alg_bytes": alg, "hbm_achieved_GBs": round(alg / (avg * 1e-3) / 1e9, 1),
+            "hbm_frac": round(alg / (avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "note": "event average; block scores, ranking, float64 block dot products and the "
+                    "ratio steps; per-sample gradients seeded N(0, 1e-2)"}
+
+
 def pct(ms, q):
     return ms[min(len(ms) - 1, int(q * (len(ms) - 1) + 0.5))]
 
@@ -309,7 +337,8 @@ def main():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
-    ap.add_argument("--no-backward", action="store_true", help="skip the backward timings")
+    ap.add_argument("--no-backward", action="store_true",
+                    help="skip the backward and delta-curve timings")
     ap.add_argument("--no-flushed", action="store_true",
                     help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
@@ -395,6 +424,7 @@ def main():
     bl = lambda: torch.addmm(b, X, W.t())
     _, bms = time_launches(bl, max(5, args.steps // 2), 3)
     back = None if args.no_backward else time_backward(w, h, W, X, args.steps, tt, to_dev)
+    dcurve = None if args.no_backward else time_delta_curve(w, W, args.steps, to_dev)
     # cold caches: the same launches after a 1 GiB write each
     fms = fdms = None
     if not args.no_flushed:
@@ -421,6 +451,10 @@ def main():
         log("backward: dX %.1f us (dense %.1f us), dW %.1f us (hipBLASLt full G^T X %.1f us), "
             "db %.1f us" % (back["dx_ms"] * 1e3, back["dx_dense_ms"] * 1e3, back["dw_ms"] * 1e3,
                             back["dw_hipblaslt_dense_ms"] * 1e3, back["db_ms"] * 1e3))
+    if dcurve:
+        log("delta curve: %.1f us for %d samples x %d points (%.0f GB/s of %d MB)"
+            % (dcurve["ms"] * 1e3, dcurve["n_samples"], dcurve["points"],
+               dcurve["hbm_achieved_GBs"], dcurve["hbm_alg_bytes"] // 1000000))
     if fms:
         log("flushed caches: bsr_linear median %.1f us, dense_linear median %.1f us (speedup %.2fx)"
             % (pct(fms, .5) * 1e3, pct(fdms, .5) * 1e3, pct(fdms, .5) / pct(fms, .5)))
@@ -458,6 +492,7 @@ def main():
             "speedup_vs_dense": round(pct(fdms, .5) / pct(fms, .5), 3),
             "note": "each launch after a 1 GiB device write (L2 and MALL evicted)"},
         "backward": back,
+        "delta_curve": dcurve,
         "pack_ms": round(pack_ms, 3),
         "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,

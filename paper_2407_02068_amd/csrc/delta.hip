@@ -13,10 +13,12 @@
 // (per-sample gradients, grad, and W itself for |d|^2) with -W over every
 // block: one pass over the per-sample gradients, which bounds the time (HBM).
 //
-//   k_block_rank   rank of each block by (-score, index) and its inverse
+//   k_rank_counts, k_rank_scatter
+//                  rank of each block by (-score, index) and its inverse
 //   k_delta_dots   float64 block dot products, one workgroup per (block-row,
 //                  vector)
-//   k_delta_curve  one workgroup: the ratio steps in rank order, the update
+//   k_delta_steps  each vector's sum over each ratio step's blocks
+//   k_delta_finish one workgroup: the update, step by step
 // All sums run in a fixed order (float64), so results do not depend on timing.
 #include "lpv_device.h"
 #include "lpv_internal.h"
@@ -26,27 +28,40 @@ namespace {
 
 // rank[b] = #{b' : score(b') > score(b), or equal and b' < b}; perm[rank[b]] = b.
 // Scores are non-negative, so their bit patterns order like their values.
-// One thread per block, the keys staged through LDS 1024 at a time.
-__global__ __launch_bounds__(256) void k_block_rank(const double* __restrict__ scores, int64_t nb,
-                                                    int32_t* __restrict__ perm)
+// k_rank_counts: thread b, chunk j of `chunk` keys (staged in LDS): the count
+// of that chunk's keys ahead of b, to cnt[j][b].  k_rank_scatter adds the
+// chunks' counts (integers: exact in any order) and writes perm.
+__global__ __launch_bounds__(256) void k_rank_counts(const double* __restrict__ scores, int64_t nb,
+                                                     int32_t chunk, int32_t* __restrict__ cnt)
 {
-    __shared__ uint64_t s_key[1024];
+    extern __shared__ uint64_t s_key[];
     const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const uint64_t key = b < nb ? (uint64_t)__double_as_longlong(scores[b]) : 0;
-    int64_t rank = 0;
-    for (int64_t base = 0; base < nb; base += 1024) {
-        __syncthreads();
-        for (int i = threadIdx.x; i < 1024; i += 256)
-            s_key[i] = base + i < nb ? (uint64_t)__double_as_longlong(scores[base + i]) : 0;
-        __syncthreads();
-        const int n = (int)min((int64_t)1024, nb - base);
-        for (int i = 0; i < n; ++i) {
-            const uint64_t k2 = s_key[i];
-            rank += (k2 > key) || (k2 == key && base + i < b);
-        }
+    const int64_t base = (int64_t)blockIdx.y * chunk;
+    const int n = (int)min((int64_t)chunk, nb - base);
+    for (int i = threadIdx.x; i < n; i += 256)
+        s_key[i] = (uint64_t)__double_as_longlong(scores[base + i]);
+    __syncthreads();
+    if (b >= nb)
+        return;
+    const uint64_t key = (uint64_t)__double_as_longlong(scores[b]);
+    int32_t r = 0;
+    for (int i = 0; i < n; ++i) {
+        const uint64_t k2 = s_key[i];
+        r += (k2 > key) || (k2 == key && base + i < b);
     }
-    if (b < nb)
-        perm[rank] = (int32_t)b;
+    cnt[(int64_t)blockIdx.y * nb + b] = r;
+}
+
+__global__ __launch_bounds__(256) void k_rank_scatter(const int32_t* __restrict__ cnt, int64_t nb,
+                                                      int32_t n_chunks, int32_t* __restrict__ perm)
+{
+    const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (b >= nb)
+        return;
+    int64_t rank = 0;
+    for (int j = 0; j < n_chunks; ++j)
+        rank += cnt[(int64_t)j * nb + b];
+    perm[rank] = (int32_t)b;
 }
 
 // The 8 elements at idx .. idx + 7 (idx a multiple of 8, 16-byte aligned) in
@@ -124,47 +139,65 @@ __global__ __launch_bounds__(256) void k_delta_dots(const DeltaCall c, int32_t C
     }
 }
 
-// One workgroup.  Step k of the curve drops the blocks of rank
-// [keep[k], keep[k - 1]) (keep[-1] = all blocks), in rank order.  Thread v
-// (a vector) walks the steps: its step sum B_k; samples keep a_v and write
-// (B_k / 2 + a_v) B_k, grad and W their step sums.  Then thread 0 adds, step by
-// step, grad . d + kappa |d|^2 / 2 + (1/N) sum_v (in order) of the samples'
-// terms.
-__global__ __launch_bounds__(1024) void k_delta_curve(const DeltaCall c, int64_t nb,
-                                                      const double* __restrict__ dots,
-                                                      const int32_t* __restrict__ perm,
-                                                      double* __restrict__ q)
+// Step sums: step k drops the blocks of rank [keep[k], keep[k - 1])
+// (keep[-1] = all blocks).  One wave per (vector v, step k): lane l adds the
+// step's blocks of rank lo + l, lo + l + 64, ... in order, then a fixed
+// butterfly adds the lanes.  bsum[k][v] = the step's sum of dots[v].
+__global__ __launch_bounds__(256) void k_delta_steps(const DeltaCall c, int64_t nb,
+                                                     const double* __restrict__ dots,
+                                                     const int32_t* __restrict__ perm,
+                                                     double* __restrict__ bsum)
 {
     const int64_t nv = c.n_samples + 2;
-    for (int64_t v = threadIdx.x; v < nv; v += 1024) {
-        const double* dv = dots + v * nb;
+    const int64_t idx = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (idx >= nv * c.n_points)
+        return;  // whole waves
+    const int lane = threadIdx.x & 63;
+    const int64_t v = idx / c.n_points;
+    const int k = (int)(idx - v * c.n_points);
+    const int64_t lo = c.keep[k], hi = k > 0 ? c.keep[k - 1] : nb;
+    const double* dv = dots + v * nb;
+    double s = 0.0;
+    for (int64_t rk = lo + lane; rk < hi; rk += 64)
+        s += dv[perm[rk]];
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1)
+        s += __shfl_xor(s, o, 64);
+    if (lane == 0)
+        bsum[(int64_t)k * nv + v] = s;
+}
+
+// One workgroup.  Sample v keeps a_v = g_v . dW_{k-1} and turns its step sums
+// into (B_k / 2 + a_v) B_k (in place); then thread k adds the samples' terms
+// in order; thread 0 adds, step by step, grad . d + kappa |d|^2 / 2 +
+// (1/N) sum_v (...).
+__global__ __launch_bounds__(1024) void k_delta_finish(const DeltaCall c, double* __restrict__ bsum,
+                                                       double* __restrict__ term)
+{
+    const int64_t nv = c.n_samples + 2;
+    for (int64_t v = threadIdx.x; v < c.n_samples; v += 1024) {
         double a = 0.0;
-        int64_t hi = nb;
         for (int k = 0; k < c.n_points; ++k) {
-            const int64_t lo = c.keep[k];
-            double bsum = 0.0;
-            for (int64_t rk = lo; rk < hi; ++rk)
-                bsum += dv[perm[rk]];
-            hi = lo;
-            if (v < c.n_samples) {
-                q[(int64_t)k * nv + v] = (0.5 * bsum + a) * bsum;
-                a += bsum;
-            } else {
-                q[(int64_t)k * nv + v] = bsum;
-            }
+            const double b = bsum[(int64_t)k * nv + v];
+            bsum[(int64_t)k * nv + v] = (0.5 * b + a) * b;
+            a += b;
         }
     }
-    __syncthreads();  // the step terms in q are visible to thread 0
+    __syncthreads();
+    for (int k = threadIdx.x; k < c.n_points; k += 1024) {
+        const double* qk = bsum + (int64_t)k * nv;
+        double f = 0.0;
+        for (int64_t v = 0; v < c.n_samples; ++v)
+            f += qk[v];
+        // grad . d, and |d|^2 = -(W . (-W)) over the step
+        term[k] = qk[c.n_samples] + 0.5 * c.kappa * -qk[c.n_samples + 1] +
+                  (c.n_samples > 0 ? f / (double)c.n_samples : 0.0);
+    }
+    __syncthreads();
     if (threadIdx.x == 0) {
         double delta = 0.0;
         for (int k = 0; k < c.n_points; ++k) {
-            const double* qk = q + (int64_t)k * nv;
-            double f = 0.0;
-            for (int64_t v = 0; v < c.n_samples; ++v)
-                f += qk[v];
-            // grad . d, then |d|^2 = -(W . (-W)) over the step
-            const double lin = qk[c.n_samples], sq = -qk[c.n_samples + 1];
-            delta += lin + 0.5 * c.kappa * sq + (c.n_samples > 0 ? f / (double)c.n_samples : 0.0);
+            delta += term[k];
             c.delta[k] = delta;
         }
     }
@@ -176,9 +209,14 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
 {
     const int32_t R = (int32_t)(c.N / c.b_r), C = (int32_t)(c.K / c.b_c);
     const int64_t nb = (int64_t)R * C, nv = c.n_samples + 2;
-    // workspace: scores (nb), dots (nv x nb), step terms (points x nv), perm (nb)
-    const size_t bytes = (size_t)(nb + nv * nb + (int64_t)c.n_points * nv) * sizeof(double) +
-                         (size_t)nb * sizeof(int32_t);
+    // ranking: keys in chunks of at least 128, at most 64 chunks
+    const int32_t chunk = (int32_t)max((int64_t)128, (nb + 63) / 64);
+    const int32_t n_chunks = (int32_t)((nb + chunk - 1) / chunk);
+    // workspace: scores (nb), dots (nv x nb), step sums (points x nv), step
+    // terms (points), perm (nb), rank counts (n_chunks x nb)
+    const size_t bytes =
+        (size_t)(nb + nv * nb + (int64_t)c.n_points * nv + c.n_points) * sizeof(double) +
+        (size_t)(nb + (int64_t)n_chunks * nb) * sizeof(int32_t);
     char* ws = nullptr;
     hipError_t e = hipMallocAsync((void**)&ws, bytes, s);
     if (e != hipSuccess)
@@ -186,13 +224,21 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
     double* scores = (double*)ws;
     double* dots = scores + nb;
     double* q = dots + nv * nb;
-    int32_t* perm = (int32_t*)(q + (int64_t)c.n_points * nv);
+    double* term = q + (int64_t)c.n_points * nv;
+    int32_t* perm = (int32_t*)(term + c.n_points);
+    int32_t* cnt = perm + nb;
     MaskCall m = {c.W, c.ldw, c.grad, c.ldg, c.N, c.K, c.dtype, c.b_r, c.b_c, 0, nullptr, scores};
     e = launch_block_scores(m, s);
     if (e == hipSuccess) {
-        hipLaunchKernelGGL(k_block_rank, dim3((unsigned)((nb + 255) / 256)), dim3(256), 0, s,
-                           (const double*)scores, nb, perm);
+        const unsigned gx = (unsigned)((nb + 255) / 256);
+        hipLaunchKernelGGL(k_rank_counts, dim3(gx, (unsigned)n_chunks), dim3(256),
+                           (size_t)chunk * sizeof(uint64_t), s, (const double*)scores, nb, chunk, cnt);
         e = hipGetLastError();
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL(k_rank_scatter, dim3(gx), dim3(256), 0, s, (const int32_t*)cnt, nb,
+                               n_chunks, perm);
+            e = hipGetLastError();
+        }
     }
     if (e == hipSuccess) {
         const dim3 grid((unsigned)R, (unsigned)nv);
@@ -207,9 +253,14 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
         e = hipGetLastError();
     }
     if (e == hipSuccess) {
-        hipLaunchKernelGGL(k_delta_curve, dim3(1), dim3(1024), 0, s, c, nb, (const double*)dots,
-                           (const int32_t*)perm, q);
+        const int64_t waves = nv * c.n_points;
+        hipLaunchKernelGGL(k_delta_steps, dim3((unsigned)((waves + 3) / 4)), dim3(256), 0, s, c, nb,
+                           (const double*)dots, (const int32_t*)perm, q);
         e = hipGetLastError();
+        if (e == hipSuccess) {
+            hipLaunchKernelGGL(k_delta_finish, dim3(1), dim3(1024), 0, s, c, q, term);
+            e = hipGetLastError();
+        }
     }
     const hipError_t ef = hipFreeAsync(ws, s);
     return e != hipSuccess ? e : ef;

@@ -31,8 +31,35 @@ template <int DT> __device__ inline double load_f64(const char* base, int64_t id
     return (double)(float)__builtin_bit_cast(_Float16, bits);
 }
 
+// 8 consecutive elements (16-byte aligned) decoded to float64, from 16-byte loads.
+template <int DT> __device__ inline void load8_f64(const char* base, int64_t idx, double* out)
+{
+    if (DT == LPV_F32) {
+        const float4 a = *(const float4*)(base + idx * 4), b = *(const float4*)(base + idx * 4 + 16);
+        out[0] = a.x, out[1] = a.y, out[2] = a.z, out[3] = a.w;
+        out[4] = b.x, out[5] = b.y, out[6] = b.z, out[7] = b.w;
+    } else {
+        const uint4 u = *(const uint4*)(base + idx * 2);
+        const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const uint16_t lo = (uint16_t)(w[j] & 0xffffu), hi = (uint16_t)(w[j] >> 16);
+            if (DT == LPV_BF16) {
+                out[2 * j] = (double)__uint_as_float((uint32_t)lo << 16);
+                out[2 * j + 1] = (double)__uint_as_float((uint32_t)hi << 16);
+            } else {
+                out[2 * j] = (double)(float)__builtin_bit_cast(_Float16, lo);
+                out[2 * j + 1] = (double)(float)__builtin_bit_cast(_Float16, hi);
+            }
+        }
+    }
+}
+
 // One thread per block (r, c) = blockIdx.x * 256 + threadIdx.x (row-major).
-template <int DT, bool TAYLOR>
+// VEC: the block's rows are read 16 bytes at a time (W and G 16-byte aligned,
+// row strides multiples of 16 bytes); the elements are still added one after
+// the other in row-major order, so the score is the same bit for bit.
+template <int DT, bool TAYLOR, bool VEC>
 __global__ __launch_bounds__(256) void k_block_scores(const char* __restrict__ W, int64_t ldw,
                                                       const char* __restrict__ G, int64_t ldg,
                                                       int64_t R, int64_t C, int32_t b_r,
@@ -46,14 +73,33 @@ __global__ __launch_bounds__(256) void k_block_scores(const char* __restrict__ W
     double s = 0.0;
     for (int32_t a = 0; a < b_r; ++a) {
         const int64_t n = r * b_r + a;
-        for (int32_t b = 0; b < b_c; ++b) {
-            const int64_t k = c * b_c + b;
-            const double w = load_f64<DT>(W, n * ldw + k);
-            if (TAYLOR) {
-                const double p = w * load_f64<DT>(G, n * ldg + k);
-                s = s + (p < 0.0 ? -p : p);
-            } else {
-                s = s + w * w;
+        if (VEC) {
+            for (int32_t b = 0; b < b_c; b += 8) {
+                const int64_t k = c * b_c + b;
+                double w[8], g[8];
+                load8_f64<DT>(W, n * ldw + k, w);
+                if (TAYLOR)
+                    load8_f64<DT>(G, n * ldg + k, g);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) {
+                    if (TAYLOR) {
+                        const double p = w[j] * g[j];
+                        s = s + (p < 0.0 ? -p : p);
+                    } else {
+                        s = s + w[j] * w[j];
+                    }
+                }
+            }
+        } else {
+            for (int32_t b = 0; b < b_c; ++b) {
+                const int64_t k = c * b_c + b;
+                const double w = load_f64<DT>(W, n * ldw + k);
+                if (TAYLOR) {
+                    const double p = w * load_f64<DT>(G, n * ldg + k);
+                    s = s + (p < 0.0 ? -p : p);
+                } else {
+                    s = s + w * w;
+                }
             }
         }
     }
@@ -137,15 +183,22 @@ hipError_t launch_block_scores(const MaskCall& m, hipStream_t s)
     const int64_t R = m.N / m.b_r, C = m.K / m.b_c, nb = R * C;
     if (nb > 0) {
         const dim3 grid((unsigned)((nb + 255) / 256)), block(256);
-#define LPV_SCORES(DT_, TY_)                                                                       \
-    hipLaunchKernelGGL((k_block_scores<DT_, TY_>), grid, block, 0, s, (const char*)m.W, m.ldw,    \
+        const int es = m.dtype == LPV_F32 ? 4 : 2;
+        const bool vec = ((uintptr_t)m.W % 16) == 0 && (m.ldw * es) % 16 == 0 &&
+                         (!m.G || (((uintptr_t)m.G % 16) == 0 && (m.ldg * es) % 16 == 0));
+#define LPV_SCORES(DT_, TY_, V_)                                                                   \
+    hipLaunchKernelGGL((k_block_scores<DT_, TY_, V_>), grid, block, 0, s, (const char*)m.W, m.ldw, \
                        (const char*)m.G, m.ldg, R, C, m.b_r, m.b_c, m.scores)
-#define LPV_SCORES_DT(DT_)                 \
-    do {                                   \
-        if (m.G)                           \
-            LPV_SCORES(DT_, true);         \
-        else                               \
-            LPV_SCORES(DT_, false);        \
+#define LPV_SCORES_DT(DT_)                   \
+    do {                                     \
+        if (m.G && vec)                      \
+            LPV_SCORES(DT_, true, true);     \
+        else if (m.G)                        \
+            LPV_SCORES(DT_, true, false);    \
+        else if (vec)                        \
+            LPV_SCORES(DT_, false, true);    \
+        else                                 \
+            LPV_SCORES(DT_, false, false);   \
     } while (0)
         if (m.dtype == LPV_BF16)
             LPV_SCORES_DT(LPV_BF16);
