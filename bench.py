@@ -297,6 +297,97 @@ def time_delta_curve(w, W, steps, to_dev):
                     "ratio steps; per-sample gradients seeded N(0, 1e-2)"}
 
 
+def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
+    """Board power in the manner of the paper's measurement (the power meter
+    averaged over a period, idle subtracted): amd-smi's socket power sampled
+    every 20 ms during an idle period, a loop of block-sparse launches and a
+    loop of dense launches (alternating, samples of each window's first
+    ``settle`` seconds dropped).  Energy per launch above idle = (power - idle)
+    x time per launch.  Beside it, the paper's power model: the within-block
+    products scale with the kept blocks.  (amd-smi's energy counter lags the
+    windows on this machine, so it is not used.)"""
+    import threading
+
+    import torch
+    try:
+        import amdsmi
+        amdsmi.amdsmi_init()
+    except Exception as e:  # no amd-smi access on this machine
+        return {"unavailable": "amdsmi: %s" % e}
+    try:
+        handles = amdsmi.amdsmi_get_processor_handles()
+        h = handles[0] if len(handles) == 1 else None
+        if h is None:
+            p = torch.cuda.get_device_properties(0)
+            want = (getattr(p, "pci_domain_id", None), getattr(p, "pci_bus_id", None),
+                    getattr(p, "pci_device_id", None))
+            for c in handles:
+                dom, bus, rest = amdsmi.amdsmi_get_gpu_device_bdf(c).split(":")
+                if (int(dom, 16), int(bus, 16), int(rest.split(".")[0], 16)) == want:
+                    h = c
+        if h is None:
+            return {"unavailable": "no amd-smi device matches the benchmarked GPU"}
+
+        def socket_w():
+            v = amdsmi.amdsmi_get_power_info(h).get("current_socket_power")
+            return float(v) if isinstance(v, (int, float)) and v > 0 else None
+
+        def window(fn):
+            samples, stop = [], threading.Event()
+            t0 = time.perf_counter()
+
+            def poll():
+                while not stop.is_set():
+                    v = socket_w()
+                    if v is not None and time.perf_counter() - t0 >= settle:
+                        samples.append(v)
+                    stop.wait(0.02)
+            th = threading.Thread(target=poll)
+            torch.cuda.synchronize()
+            th.start()
+            n = 0
+            if fn is None:
+                time.sleep(seconds)
+            else:
+                while time.perf_counter() - t0 < seconds:
+                    for _ in range(50):
+                        fn()
+                    n += 50
+                    torch.cuda.synchronize()
+            el = time.perf_counter() - t0
+            stop.set()
+            th.join()
+            if not samples:
+                raise RuntimeError("no power samples")
+            return sum(samples) / len(samples), n, el
+
+        runs = {"idle": [], "bsr": [], "dense": []}
+        for kind, fn in (("idle", None), ("bsr", sparse), ("dense", dense), ("bsr", sparse),
+                         ("dense", dense), ("idle", None)):
+            runs[kind].append(window(fn))
+        watts = {k: sum(r[0] for r in v) / len(v) for k, v in runs.items()}
+        per_launch_s = {k: sum(r[2] for r in v) / sum(r[1] for r in v) for k, v in runs.items()
+                        if k != "idle"}
+        e = {k: (watts[k] - watts["idle"]) * per_launch_s[k] * 1e3 for k in per_launch_s}  # mJ
+        return {"idle_W": round(watts["idle"], 1), "bsr_W": round(watts["bsr"], 1),
+                "dense_W": round(watts["dense"], 1),
+                "bsr_mJ_per_launch_above_idle": round(e["bsr"], 2),
+                "dense_mJ_per_launch_above_idle": round(e["dense"], 2),
+                "energy_reduction_pct": round(100.0 * (1.0 - e["bsr"] / e["dense"]), 1)
+                if e["dense"] > 0 else None,
+                "power_model_kept_fraction": round(w.nnzb / w.mask.size, 4),
+                "method": "amd-smi current socket power every 20 ms over %.1f s windows "
+                          "(idle, block-sparse, dense, block-sparse, dense, idle; first %.1f s "
+                          "of each dropped)" % (seconds, settle)}
+    except Exception as e:
+        return {"unavailable": "amdsmi: %s" % e}
+    finally:
+        try:
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
+
+
 def pct(ms, q):
     return ms[min(len(ms) - 1, int(q * (len(ms) - 1) + 0.5))]
 
@@ -339,6 +430,7 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the backward and delta-curve timings")
+    ap.add_argument("--no-power", action="store_true", help="skip the amd-smi power leg")
     ap.add_argument("--no-flushed", action="store_true",
                     help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
@@ -425,6 +517,7 @@ def main():
     _, bms = time_launches(bl, max(5, args.steps // 2), 3)
     back = None if args.no_backward else time_backward(w, h, W, X, args.steps, tt, to_dev)
     dcurve = None if args.no_backward else time_delta_curve(w, W, args.steps, to_dev)
+    power = None if args.no_power else measure_power(sparse, dense, w)
     # cold caches: the same launches after a 1 GiB write each
     fms = fdms = None
     if not args.no_flushed:
@@ -451,6 +544,8 @@ def main():
         log("backward: dX %.1f us (dense %.1f us), dW %.1f us (hipBLASLt full G^T X %.1f us), "
             "db %.1f us" % (back["dx_ms"] * 1e3, back["dx_dense_ms"] * 1e3, back["dw_ms"] * 1e3,
                             back["dw_hipblaslt_dense_ms"] * 1e3, back["db_ms"] * 1e3))
+    if power:
+        log("power: %s" % json.dumps(power))
     if dcurve:
         log("delta curve: %.1f us for %d samples x %d points (%.0f GB/s of %d MB)"
             % (dcurve["ms"] * 1e3, dcurve["n_samples"], dcurve["points"],
@@ -493,6 +588,7 @@ def main():
             "note": "each launch after a 1 GiB device write (L2 and MALL evicted)"},
         "backward": back,
         "delta_curve": dcurve,
+        "power": power,
         "pack_ms": round(pack_ms, 3),
         "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
