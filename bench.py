@@ -27,6 +27,7 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E (published)
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "bsr_linear_fc1_hbm_traffic.json")
 CLOCK_FILE = os.path.join(ROOT, "profiles", "bsr_linear_fc1_gpu_clock.md")
 STATS_FILE = os.path.join(ROOT, "profiles", "bsr_linear_deit_b_fc1_bf16_kernel_stats.md")
+STATS_FILE_BACKWARD = os.path.join(ROOT, "profiles", "backward_delta_deit_b_fc1_bf16_kernel_stats.md")
 KERNEL_SOURCES = ("paper_2407_02068_amd/csrc/linear.hip", "paper_2407_02068_amd/csrc/lpv_device.h",
                   "paper_2407_02068_amd/csrc/lpv_internal.h")
 
@@ -110,7 +111,14 @@ def kernel_label(name):
     """A short name for a kernel of the rocprofv3 statistics."""
     labels = ((SPARSE_KERNEL, "k_linear16 bf16 block-sparse (lpv_bsr_linear)"),
               (DENSE_KERNEL, "k_linear16 bf16 dense (lpv_dense_linear)"),
+              ("k_block_scores<2, true", "k_block_scores, Taylor (lpv_delta_curve)"),
+              ("k_block_scores<2, false", "k_block_scores, sum of squares (lpv_mask_topk)"),
               ("k_block_scores", "k_block_scores (lpv_mask_topk)"),
+              ("k_delta_dots", "k_delta_dots (lpv_delta_curve)"),
+              ("k_rank_counts", "k_rank_counts (lpv_delta_curve)"),
+              ("k_rank_scatter", "k_rank_scatter (lpv_delta_curve)"),
+              ("k_delta_steps", "k_delta_steps (lpv_delta_curve)"),
+              ("k_delta_finish", "k_delta_finish (lpv_delta_curve)"),
               ("k_mask_topk", "k_mask_topk (lpv_mask_topk)"),
               ("FillFunctor", "torch fill (cache flush between cold launches)"))
     for key, label in labels:
@@ -128,16 +136,23 @@ def kernel_label(name):
     return name.split("(")[0][:72]
 
 
-def write_stats(stats_csv, command):
+STATS_RUN = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
+             "-- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed --no-power --no-backward")
+STATS_RUN_BACKWARD = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bw -o bw --output-format "
+                      "csv -- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed --no-power")
+
+
+def write_stats(stats_csv, command, backward=False):
     """The rocprofv3 --kernel-trace --stats summary of a bench.py run as a
-    short table next to the other profiles."""
+    short table next to the other profiles: the forward run, or (backward)
+    the run with the backward and delta-curve legs."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
     text = ["# rocprofv3 kernel statistics: DeiT-B fc1 (X 50432 x 768 -> 3072), bf16, 32x32 blocks, "
-            "50% block sparsity, forward and backward", "",
+            "50%% block sparsity, %s" % ("forward, backward and delta curve" if backward else
+                                         "forward"), "",
             "Profiled run, then this summary (from the repository root on one MI355X):", "", "```",
-            "rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
-            "-- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed", command, "```", "",
+            STATS_RUN_BACKWARD if backward else STATS_RUN, command, "```", "",
             "| kernel | calls | avg us | min us | max us | % of GPU time |",
             "|---|---:|---:|---:|---:|---:|"]
     for r in rows:
@@ -145,19 +160,22 @@ def write_stats(stats_csv, command):
             kernel_label(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
     sp = [r for r in rows if SPARSE_KERNEL in r["Name"]]
-    if sp:
+    if backward:
+        text += ["", "The block-sparse k_linear16 row counts the forward launches and the dX "
+                 "launches (the same kernel on the transposed handle).  dW is k_gradw_tiles + "
+                 "k_gradw_reduce, db k_bias_partial + k_bias_reduce, the delta curve "
+                 "k_block_scores + k_rank_counts + k_rank_scatter + k_delta_dots + "
+                 "k_delta_steps + k_delta_finish; Cijk_Ailk is hipBLASLt's dense G^T X "
+                 "reference, Custom_Cijk_Alik its dense forward."]
+    elif sp:
         avg_us = float(sp[0]["AverageNs"]) / 1e3
         text += ["", "The hipBLASLt row (Cijk) is `torch.addmm` at the same shape, a check on the "
                  "dense path.  Kept work of one block-sparse launch: 118.98 GFLOP, so the "
                  "block-sparse average above is %.0f TFLOP/s (%.1f%% of the 2.5 PFLOP/s bf16 "
                  "matrix-core peak); `bench.py` times the same launches with HIP events on their "
-                 "stream and reports that average as `roofline.achieved`.  The backward rows: "
-                 "dX is the block-sparse forward kernel on the transposed handle (its calls "
-                 "are counted with the forward's), dW is k_gradw_tiles + k_gradw_reduce, db is "
-                 "k_bias_partial + k_bias_reduce; the second hipBLASLt kernel (Cijk_Ailk) is "
-                 "the dense G^T X reference."
+                 "stream and reports that average as `roofline.achieved`."
                  % (118.98e9 / (avg_us * 1e-6) / 1e12, 118.98e9 / (avg_us * 1e-6) / 1e12 / 25.0)]
-    with open(STATS_FILE, "w") as f:
+    with open(STATS_FILE_BACKWARD if backward else STATS_FILE, "w") as f:
         f.write("\n".join(text) + "\n")
     print("\n".join(text))
 
@@ -443,6 +461,8 @@ def main():
                     help="turn two --profile-pass counter CSVs into the HBM traffic summary")
     ap.add_argument("--write-stats", metavar="STATS_CSV",
                     help="turn a rocprofv3 --stats kernel CSV of this script into the statistics summary")
+    ap.add_argument("--write-stats-backward", metavar="STATS_CSV",
+                    help="the same for the run with the backward and delta-curve legs")
     ap.add_argument("--write-clock", metavar="CLOCK_CSV",
                     help="turn a --profile-pass GRBM_GUI_ACTIVE counter CSV into the clock summary")
     args = ap.parse_args()
@@ -452,6 +472,10 @@ def main():
         return
     if args.write_stats:
         write_stats(args.write_stats, command=" ".join(["python bench.py"] + sys.argv[1:]))
+        return
+    if args.write_stats_backward:
+        write_stats(args.write_stats_backward,
+                    command=" ".join(["python bench.py"] + sys.argv[1:]), backward=True)
         return
     if args.write_clock:
         write_clock(args.write_clock, command=" ".join(["python bench.py"] + sys.argv[1:]))
