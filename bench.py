@@ -137,9 +137,9 @@ def kernel_label(name):
 
 
 STATS_RUN = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
-             "-- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed --no-power --no-backward")
+             "-- python bench.py --no-cpu --no-flushed --no-power --no-backward")
 STATS_RUN_BACKWARD = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bw -o bw --output-format "
-                      "csv -- python bench.py --steps 30 --warmup 5 --no-cpu --no-flushed --no-power")
+                      "csv -- python bench.py --no-cpu --no-flushed --no-power")
 
 
 def write_stats(stats_csv, command, backward=False):
@@ -443,8 +443,9 @@ def cpu_baseline(w, target_s=12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=100)
+    # defaults: the clock settles within the 2000 untimed launches (~0.4 s)
+    ap.add_argument("--steps", type=int, default=500)
+    ap.add_argument("--warmup", type=int, default=2000)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the backward and delta-curve timings")
@@ -538,7 +539,7 @@ def main():
     dwall, dms = time_launches(dense, args.steps, args.warmup)
     # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
     bl = lambda: torch.addmm(b, X, W.t())
-    _, bms = time_launches(bl, max(5, args.steps // 2), 3)
+    _, bms = time_launches(bl, args.steps, args.warmup)
     back = None if args.no_backward else time_backward(w, h, W, X, args.steps, tt, to_dev)
     dcurve = None if args.no_backward else time_delta_curve(w, W, args.steps, to_dev)
     power = None if args.no_power else measure_power(sparse, dense, w)
@@ -605,6 +606,7 @@ def main():
         "bsr_ms_p10": round(pct(ms, .1), 5),
         "bsr_ms_p90": round(pct(ms, .9), 5),
         "hipblaslt_addmm_ms": round(pct(bms, .5), 5),
+        "speedup_vs_hipblaslt": round(pct(bms, .5) / pct(ms, .5), 3),
         "flushed": None if not fms else {
             "bsr_ms_median": round(pct(fms, .5), 5), "bsr_ms_p90": round(pct(fms, .9), 5),
             "dense_ms_median": round(pct(fdms, .5), 5),
