@@ -495,8 +495,8 @@ hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, in
 {
     const int V = dtype == LPV_F32 ? 4 : 8;
     const int64_t bx = (N + 256 * V - 1) / (256 * V);
-    // about 1024 workgroups of 8 waves, at least 64 rows each
-    int64_t n_chunks = (1024 + bx - 1) / bx;
+    // about 512 workgroups (two per compute unit), at least 64 rows each
+    int64_t n_chunks = (512 + bx - 1) / bx;
     n_chunks = max((int64_t)1, min(n_chunks, (M + 63) / 64));
     const int64_t rows = (M + n_chunks - 1) / n_chunks;
     n_chunks = M > 0 ? (M + rows - 1) / rows : 1;
