@@ -76,3 +76,10 @@ def test_delta_curve_headline_layer():
     grad = wl.quantize(g.normal(0, 1e-3, w.W.shape).astype(np.float32), "bf16")
     S = wl.quantize(g.normal(0, 1e-2, (8,) + w.W.shape).astype(np.float32), "bf16")
     check(w.W, grad, S, "bf16", 32, 32, 1e-4, [0, 30, 50, 70], "b_fc1")
+
+
+def test_delta_curve_widest_rows():
+    # K = 65536, the widest weight: the block dot kernel's chunk sums fill
+    # 64 KB of LDS
+    W, grad, S = inputs(106, 16, 65536, 2, "bf16")
+    check(W, grad, S, "bf16", 16, 16, 0.01, [0, 50, 100], "K = 65536")
