@@ -192,8 +192,8 @@ __global__ __launch_bounds__(256) void k_gradw_plain(int32_t b_r, int32_t b_c, i
 // outputs n) times 8 tile columns (256 inputs k) -- and a chunk of tokens, and
 // computes for every kept 32 x 32 tile of the window the partial product
 // G[chunk, tile rows]^T X[chunk, tile columns] with the matrix cores.  Tokens
-// are the reduction: they stream through a 4-stage LDS ring, 32 per stage
-// (G: 32 x 256 and X: 32 x 256 elements, 16 KB each, rows of 512 bytes whose
+// are the reduction: they stream through a 2-stage LDS ring, 64 per stage
+// (G: 64 x 256 and X: 64 x 256 elements, 32 KB each, rows of 512 bytes whose
 // 64-byte segments are XOR-swizzled by the row).  The MFMA operands need 8
 // consecutive tokens per lane; ds_read_b64_tr_b16 gathers them from the
 // token-major rows: within each 16-lane group, lane i receives element i % 4
@@ -209,8 +209,12 @@ __global__ __launch_bounds__(256) void k_gradw_plain(int32_t b_r, int32_t b_c, i
 // Partials go to ws[chunk][tile row][tile col][1024] in accumulator order
 // (lane-major float4 runs); k_gradw_reduce adds the chunks in order.
 constexpr int GW_NT = 512;
-constexpr int GW_STAGE = 32768;  // bytes: G 16 KB + X 16 KB
-constexpr int GW_NSTG = 4;
+constexpr int GW_TOK = 64;                   // tokens per step
+constexpr int GW_KS = GW_TOK / 16;           // matrix-core k-steps per step
+constexpr int GW_XOFF = GW_TOK * 512;        // bytes of a stage's G part (then X)
+constexpr int GW_STAGE = 2 * GW_XOFF;        // one stage: 64 KB
+constexpr int GW_NSTG = 2;
+constexpr int GW_DMA = GW_TOK / 16;          // DMA instructions per wave and part
 
 struct GradWDims {
     int64_t M, ldg, ldx, N, K;
@@ -336,37 +340,38 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
     // (two 1 KB instructions each); LDS chunk q (16 bytes) of row r holds
     // columns 32 (seg ^ swz(r)) + 8 (q % 4) .. + 7 with seg = q / 4.
     const uint32_t smem0 = lds_u32(smem);
-    int drow[2];
-    int64_t gcol[2], xcol[2];
+    int drow[GW_DMA];
+    int64_t gcol[GW_DMA], xcol[GW_DMA];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-        drow[i] = 4 * wave + 2 * i + (lane >> 5);
+    for (int i = 0; i < GW_DMA; ++i) {
+        drow[i] = (GW_TOK / 8) * wave + 2 * i + (lane >> 5);
         const int q = lane & 31;
         const int col = 32 * ((q >> 2) ^ gw_swz(drow[i])) + 8 * (q & 3);
         gcol[i] = min((int64_t)g * 256 + col, d.N - 8);  // past the edge: any valid
         xcol[i] = min((int64_t)wc * 256 + col, d.K - 8);  // columns (never kept)
     }
-    const int64_t n_steps = (m_end - m_begin + 31) / 32;
+    const int64_t n_steps = (m_end - m_begin + GW_TOK - 1) / GW_TOK;
     // issue the DMA of token step st into its stage
     auto dma_step = [&](int64_t st) {
-        const uint32_t base = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE + (uint32_t)wave * 2048;
+        const uint32_t base = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE +
+                              (uint32_t)wave * (GW_TOK / 8) * 512;
 #pragma unroll
-        for (int i = 0; i < 2; ++i) {
-            const int64_t m = m_begin + st * 32 + drow[i];
+        for (int i = 0; i < GW_DMA; ++i) {
+            const int64_t m = m_begin + st * GW_TOK + drow[i];
             const char* gs = m < m_end ? G + (m * d.ldg + gcol[i]) * 2 : (const char*)g_zero_line;
             const char* xs = X + (min(m, d.M - 1) * d.ldx + xcol[i]) * 2;
             gw_dma(gs, base + i * 1024);
-            gw_dma(xs, base + 16384 + i * 1024);
+            gw_dma(xs, base + GW_XOFF + i * 1024);
         }
     };
 
     // transposed operand reads: (k-step ks, half h) -> row and byte offset
     // within the row; the segment is the tile row (G) or tile column (X)
-    uint32_t roff[2][2], rswz[2][2];
+    uint32_t roff[GW_KS][2], rswz[GW_KS][2];
     {
         const int q16 = lane >> 4, j16 = lane & 15;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks)
+        for (int ks = 0; ks < GW_KS; ++ks)
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const int row = ks * 16 + 8 * (q16 >> 1) + 4 * h + (j16 >> 2);
@@ -387,25 +392,18 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
     for (int t = 0; t < 8; ++t)
         acc[t] = f32x16{};
 
-    // prologue: steps 0, 1, 2
-    for (int64_t st = 0; st < 3 && st < n_steps; ++st)
-        dma_step(st);
+    // prologue: step 0
+    dma_step(0);
     for (int64_t st = 0; st < n_steps; ++st) {
-        // step st has landed for this wave once at most the DMA of the steps
-        // after it (4 instructions each) is in flight; then the barrier
-        // publishes it to everyone and frees the stage of step st - 1
-        const int64_t ahead = min((int64_t)2, n_steps - 1 - st);
-        if (ahead == 2)
-            asm volatile("s_waitcnt vmcnt(8)\n s_barrier" ::: "memory");
-        else if (ahead == 1)
-            asm volatile("s_waitcnt vmcnt(4)\n s_barrier" ::: "memory");
-        else
-            asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory");
-        if (st + 3 < n_steps)
-            dma_step(st + 3);
+        // step st's DMA (the wave's only one in flight) has landed; the
+        // barrier publishes it to everyone and frees the stage of step st - 1,
+        // which then receives step st + 1
+        asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory");
+        if (st + 1 < n_steps)
+            dma_step(st + 1);
         const uint32_t stage = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
+        for (int ks = 0; ks < GW_KS; ++ks) {
             // one G fragment for the row, one X fragment per kept tile, each
             // in registers of its own; then the products
             const F a = frag(stage, ks, tj);
@@ -413,7 +411,7 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
 #pragma unroll
             for (int t = 0; t < 8; ++t)
                 if (t < n_w)
-                    b[t] = frag(stage + 16384, ks, tc[t]);
+                    b[t] = frag(stage + GW_XOFF, ks, tc[t]);
 #pragma unroll
             for (int t = 0; t < 8; ++t)
                 if (t < n_w)
@@ -562,8 +560,8 @@ hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
     const int64_t n_win = (int64_t)d.n_groups * d.n_wcols;
     // about one workgroup per compute unit; chunks of whole 32-token steps
     int64_t n_chunks = max((int64_t)1, (int64_t)device_cus() / n_win);
-    n_chunks = min(n_chunks, (c.M + 31) / 32);
-    d.chunk_rows = ((c.M + n_chunks - 1) / n_chunks + 31) / 32 * 32;
+    n_chunks = min(n_chunks, (c.M + GW_TOK - 1) / GW_TOK);
+    d.chunk_rows = ((c.M + n_chunks - 1) / n_chunks + GW_TOK - 1) / GW_TOK * GW_TOK;
     d.n_chunks = (int32_t)((c.M + d.chunk_rows - 1) / d.chunk_rows);
     const int64_t chunk_stride = (int64_t)d.n_tile_rows * d.n_tile_cols * 1024;
     float* ws = nullptr;
