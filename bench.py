@@ -406,6 +406,57 @@ def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
             pass
 
 
+def time_stack(steps, to_dev):
+    """The DeiT-B linear stack at batch 256: 12 layers of qkv -> proj -> fc1 +
+    GELU -> fc2, each at its own sparsity (uniform in [30, 80]%, Zipf-skewed
+    rows), chained on the GPU (proj reads the V third of qkv in place).  Kept
+    TFLOP/s of the whole chain, beside the same chain through the library's
+    dense kernel."""
+    import torch
+
+    import workloads as wl
+    from paper_2407_02068_amd import lpv
+    layers = wl.b_stack()
+    M = layers[0].M
+    hs = [lpv.bsr_pack(to_dev(w.W), torch.from_numpy(w.mask).cuda(), w.b_r, w.b_c) for w in layers]
+    Wd = [to_dev(w.W) for w in layers]
+    bs = [to_dev(w.bias) for w in layers]
+    X0 = to_dev(layers[0].X)
+    tt = X0.dtype
+    qkv = torch.empty((M, 2304), dtype=tt, device="cuda")
+    P = torch.empty((M, 768), dtype=tt, device="cuda")
+    H = torch.empty((M, 3072), dtype=tt, device="cuda")
+    Xs = [torch.empty((M, 768), dtype=tt, device="cuda") for _ in range(2)]
+
+    def chain(sparse):
+        x = X0
+        for l in range(len(layers) // 4):
+            ws = range(4 * l, 4 * l + 4)
+            outs = (qkv, P, H, Xs[l % 2])
+            ins = (x, qkv[:, 1536:], P, H)
+            for i, j in enumerate(ws):
+                epi = "gelu" if layers[j].gelu else None
+                if sparse:
+                    lpv.bsr_linear(hs[j], ins[i], bs[j], outs[i], epi=epi)
+                else:
+                    lpv.dense_linear(Wd[j], ins[i], bs[j], outs[i], epi=epi)
+            x = Xs[l % 2]
+
+    n = max(5, steps // 50)
+    _, sms = time_launches(lambda: chain(True), n, 3)
+    _, dms = time_launches(lambda: chain(False), n, 3)
+    for h in hs:
+        h.close()
+    kept = sum(w.kept_flops() for w in layers)
+    dense = sum(w.dense_flops() for w in layers)
+    avg = lambda ms: sum(ms) / len(ms)
+    return {"layers": len(layers) // 4, "linears": len(layers),
+            "kept_gflop": round(kept / 1e9, 1), "dense_gflop": round(dense / 1e9, 1),
+            "ms": round(avg(sms), 4), "tflops": round(kept / (avg(sms) * 1e-3) / 1e12, 1),
+            "dense_ms": round(avg(dms), 4), "speedup_vs_dense": round(avg(dms) / avg(sms), 3),
+            "note": "event averages of the whole chain; DeiT-B, 50432 tokens, 32x32 blocks"}
+
+
 def pct(ms, q):
     return ms[min(len(ms) - 1, int(q * (len(ms) - 1) + 0.5))]
 
@@ -450,6 +501,7 @@ def main():
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the backward and delta-curve timings")
     ap.add_argument("--no-power", action="store_true", help="skip the amd-smi power leg")
+    ap.add_argument("--no-stack", action="store_true", help="skip the 12-layer DeiT-B stack")
     ap.add_argument("--no-flushed", action="store_true",
                     help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
@@ -543,6 +595,7 @@ def main():
     back = None if args.no_backward else time_backward(w, h, W, X, args.steps, tt, to_dev)
     dcurve = None if args.no_backward else time_delta_curve(w, W, args.steps, to_dev)
     power = None if args.no_power else measure_power(sparse, dense, w)
+    stack = None if args.no_stack else time_stack(args.steps, to_dev)
     # cold caches: the same launches after a 1 GiB write each
     fms = fdms = None
     if not args.no_flushed:
@@ -571,6 +624,10 @@ def main():
                             back["dw_hipblaslt_dense_ms"] * 1e3, back["db_ms"] * 1e3))
     if power:
         log("power: %s" % json.dumps(power))
+    if stack:
+        log("DeiT-B linear stack: %.2f ms per chain of %d linears (%.0f TFLOP/s kept), dense "
+            "%.2f ms (speedup %.2fx)" % (stack["ms"], stack["linears"], stack["tflops"],
+                                         stack["dense_ms"], stack["speedup_vs_dense"]))
     if dcurve:
         log("delta curve: %.1f us for %d samples x %d points (%.0f GB/s of %d MB)"
             % (dcurve["ms"] * 1e3, dcurve["n_samples"], dcurve["points"],
@@ -615,6 +672,7 @@ def main():
         "backward": back,
         "delta_curve": dcurve,
         "power": power,
+        "stack": stack,
         "pack_ms": round(pack_ms, 3),
         "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,
