@@ -137,9 +137,9 @@ def kernel_label(name):
 
 
 STATS_RUN = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
-             "-- python bench.py --no-cpu --no-flushed --no-power --no-backward")
+             "-- python bench.py --no-cpu --no-flushed --no-power --no-backward --no-stack")
 STATS_RUN_BACKWARD = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bw -o bw --output-format "
-                      "csv -- python bench.py --no-cpu --no-flushed --no-power")
+                      "csv -- python bench.py --no-cpu --no-flushed --no-power --no-stack")
 
 
 def write_stats(stats_csv, command, backward=False):
