@@ -295,6 +295,48 @@ const char* lpv_status_str(lpv_status s);
 /* Detail of the calling thread's last failed call ("" if none). */
 const char* lpv_last_error(void);
 
+/* ------------------------------------------------------------------------
+ * The encoder block around the pruned layers.  The paper prunes the linear
+ * layers of DeiT / Swin encoder blocks (Sec. 4) and measures whole models
+ * (Tab. 2); these two calls are the rest of a pre-norm block (LN -> qkv ->
+ * attention -> proj -> residual -> LN -> fc1 + GELU -> fc2 -> residual), so
+ * the block can run on the GPU with the block-sparse layers in place.  16-bit
+ * element types only (DTYPE otherwise).
+ * ------------------------------------------------------------------------ */
+
+/*
+ * lpv_add_layernorm -- per row of M rows of D elements (row-major, rows
+ * contiguous): s = x + y (y may be NULL: s = x), and
+ *   out = (s - mean(s)) / sqrt(var(s) + eps) * gamma + beta,
+ * var the biased variance over the row.  s is formed, and the statistics
+ * taken, in float32; s is written, rounded, to S when S is not NULL.
+ * x, y, S, out: device, M x D, 8-byte aligned; S and out may alias x or y.
+ * gamma, beta: device, D elements, 8-byte aligned.  4 <= D <= 2048, D a
+ * multiple of 4; 0 <= M < 2^31; eps finite and >= 0.  No host
+ * synchronisation, no allocation.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, HIP.
+ */
+lpv_status lpv_add_layernorm(const void* x, const void* y, int64_t M, int64_t D, lpv_dtype dt,
+                             const void* gamma, const void* beta, double eps, void* S, void* out,
+                             void* stream);
+
+/*
+ * lpv_attention -- multi-head self-attention of n_seq sequences of T tokens:
+ * for every sequence and head h, out_h = softmax(Q_h K_h^T / sqrt(hd)) V_h.
+ * qkv: device, (n_seq T) x (3 H hd) row-major, the qkv layer's output: row t
+ *      holds q, then k, then v, each H heads of hd contiguous elements.
+ * out: device, (n_seq T) x (H hd), head h in columns h hd .. h hd + hd - 1;
+ *      must not overlap qkv.
+ * Float32 scores and accumulation (matrix cores); the softmax weights are
+ * rounded once to the element type and the output divided by their sum.
+ * hd = 64; 1 <= T <= 512; 1 <= H <= 64; n_seq >= 0 with n_seq T and n_seq H
+ * below 2^31.  qkv and out 16-byte aligned.  No host synchronisation, no
+ * allocation.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, ALIAS (out overlaps qkv), HIP.
+ */
+lpv_status lpv_attention(const void* qkv, int64_t n_seq, int32_t T, int32_t H, int32_t hd,
+                         lpv_dtype dt, void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -11,7 +11,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblpv.so")
-SOURCES = ["api.hip", "pack.hip", "linear.hip", "mask.hip", "backward.hip", "delta.hip"]
+SOURCES = ["api.hip", "pack.hip", "linear.hip", "mask.hip", "backward.hip", "delta.hip", "encoder.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

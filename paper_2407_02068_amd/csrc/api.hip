@@ -8,6 +8,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <cmath>
 #include <new>
 
 #include "lpv_internal.h"
@@ -618,3 +619,51 @@ void lpv_bsr_destroy(lpv_bsr* h)
 }
 
 }  // extern "C"
+
+lpv_status lpv_add_layernorm(const void* x, const void* y, int64_t M, int64_t D, lpv_dtype dt,
+                             const void* gamma, const void* beta, double eps, void* S, void* out,
+                             void* stream)
+{
+    if (dt != LPV_BF16 && dt != LPV_F16)
+        return fail(LPV_ERR_DTYPE, "add_layernorm takes 16-bit element types only (got %d)", (int)dt);
+    if (D < 4 || D > lpv::LN_MAX_D || D % 4)
+        return fail(LPV_ERR_SHAPE, "D = %lld must be a multiple of 4 in [4, %d]", (long long)D,
+                    lpv::LN_MAX_D);
+    if (M < 0 || M >= MAX_M)
+        return fail(LPV_ERR_SHAPE, "M = %lld is out of range [0, 2^31)", (long long)M);
+    if (!(eps >= 0.0) || !std::isfinite(eps))
+        return fail(LPV_ERR_INVALID_ARG, "eps must be finite and >= 0");
+    auto a8 = [](const void* p) { return ((uintptr_t)p & 7u) == 0; };
+    if (!gamma || !beta || !a8(gamma) || !a8(beta))
+        return fail(LPV_ERR_INVALID_ARG, "gamma and beta must be non-NULL and 8-byte aligned");
+    if (M > 0 && (!x || !out || !a8(x) || !a8(out) || (y && !a8(y)) || (S && !a8(S))))
+        return fail(LPV_ERR_INVALID_ARG, "x, y, S and out must be 8-byte aligned (x, out non-NULL)");
+    hipError_t e = lpv::launch_add_layernorm(x, y, M, (int32_t)D, dt, gamma, beta, (float)eps, S,
+                                             out, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "add_layernorm launch");
+}
+
+lpv_status lpv_attention(const void* qkv, int64_t n_seq, int32_t T, int32_t H, int32_t hd,
+                         lpv_dtype dt, void* out, void* stream)
+{
+    if (dt != LPV_BF16 && dt != LPV_F16)
+        return fail(LPV_ERR_DTYPE, "attention takes 16-bit element types only (got %d)", (int)dt);
+    if (hd != lpv::ATT_HD)
+        return fail(LPV_ERR_SHAPE, "head dimension %d is not supported (only %d)", hd, lpv::ATT_HD);
+    if (T < 1 || T > lpv::ATT_MAX_T)
+        return fail(LPV_ERR_SHAPE, "T = %d is out of range [1, %d]", T, lpv::ATT_MAX_T);
+    if (H < 1 || H > 64)
+        return fail(LPV_ERR_SHAPE, "H = %d is out of range [1, 64]", H);
+    if (n_seq < 0 || n_seq * T >= MAX_M || n_seq * H >= MAX_M)
+        return fail(LPV_ERR_SHAPE, "n_seq = %lld is out of range", (long long)n_seq);
+    if (n_seq > 0) {
+        if (!qkv || !out || !aligned16(qkv) || !aligned16(out))
+            return fail(LPV_ERR_INVALID_ARG, "qkv and out must be non-NULL and 16-byte aligned");
+        const uintptr_t q0 = (uintptr_t)qkv, q1 = q0 + (uintptr_t)(n_seq * T * 3 * H * hd * 2);
+        const uintptr_t o0 = (uintptr_t)out, o1 = o0 + (uintptr_t)(n_seq * T * H * hd * 2);
+        if (o0 < q1 && q0 < o1)
+            return fail(LPV_ERR_ALIAS, "out must not overlap qkv");
+    }
+    hipError_t e = lpv::launch_attention(qkv, n_seq, T, H, dt, out, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "attention launch");
+}

@@ -22,7 +22,7 @@ EPI = {None: 0, "none": 0, "gelu": 1}
 EXPORTED = ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
             "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
             "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_delta_curve",
-            "lpv_bsr_destroy", "lpv_status_str", "lpv_last_error")
+            "lpv_add_layernorm", "lpv_attention", "lpv_bsr_destroy", "lpv_status_str", "lpv_last_error")
 
 
 class LpvError(RuntimeError):
@@ -67,6 +67,8 @@ def lib():
     L.lpv_bsr_transpose.argtypes = [vp, vp, ctypes.POINTER(vp)]
     L.lpv_bsr_grad_w.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.lpv_bias_grad.argtypes = [vp, i64, i64, i64, i32, vp, vp]
+    L.lpv_add_layernorm.argtypes = [vp, vp, i64, i64, i32, vp, vp, ctypes.c_double, vp, vp, vp]
+    L.lpv_attention.argtypes = [vp, i64, i32, i32, i32, i32, vp, vp]
     L.lpv_delta_curve.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, vp, i64, i64, i64,
                                   ctypes.c_double, vp, i32, vp, vp]
     for f in ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
@@ -351,3 +353,45 @@ def delta_curve(W, grad, samples, b_r, b_c, kappa, pcts, out=None, stream=None):
                                  pc, len(pcts), ctypes.c_void_p(out.data_ptr()), _stream(stream)),
            "lpv_delta_curve")
     return out
+
+
+def _vec(t, name, dtype, n):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != dtype or t.numel() != n \
+            or not t.is_contiguous():
+        raise ValueError("%s must be a contiguous %s GPU tensor of %d elements" % (name, dtype, n))
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def add_layernorm(x, y, gamma, beta, eps, S=None, out=None, stream=None):
+    """lpv_add_layernorm: s = x + y (y may be None), out = LN(s) * gamma + beta
+    per row; s is written to S when given.  x, y, S, out: contiguous M x D."""
+    if x.dim() != 2 or not x.is_contiguous():
+        raise ValueError("x must be a contiguous 2-D tensor")
+    M, D = x.shape
+    if out is None:
+        out = torch.empty_like(x)
+    for t, n in ((y, "y"), (S, "S"), (out, "out")):
+        if t is not None and (t.shape != x.shape or t.dtype != x.dtype or not t.is_contiguous()):
+            raise ValueError("%s must be a contiguous tensor shaped and typed like x" % n)
+    ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
+    _check(lib().lpv_add_layernorm(ptr(x), ptr(y), M, D, DTYPES[x.dtype],
+                                   _vec(gamma, "gamma", x.dtype, D), _vec(beta, "beta", x.dtype, D),
+                                   float(eps), ptr(S), ptr(out), _stream(stream)),
+           "lpv_add_layernorm")
+    return out
+
+
+def attention(qkv, n_seq, T, H, out=None, stream=None, hd=64):
+    """lpv_attention: multi-head self-attention of n_seq sequences of T tokens
+    from the qkv layer's output ((n_seq T) x (3 H hd), contiguous); returns
+    (n_seq T) x (H hd)."""
+    if qkv.dim() != 2 or not qkv.is_contiguous() or tuple(qkv.shape) != (n_seq * T, 3 * H * hd):
+        raise ValueError("qkv must be a contiguous (n_seq T) x (3 H hd) tensor")
+    if out is None:
+        out = torch.empty((n_seq * T, H * hd), dtype=qkv.dtype, device=qkv.device)
+    if tuple(out.shape) != (n_seq * T, H * hd) or out.dtype != qkv.dtype or not out.is_contiguous():
+        raise ValueError("out must be a contiguous (n_seq T) x (H hd) tensor of qkv's dtype")
+    _check(lib().lpv_attention(ctypes.c_void_p(qkv.data_ptr()), n_seq, T, H, hd, DTYPES[qkv.dtype],
+                               ctypes.c_void_p(out.data_ptr()), _stream(stream)), "lpv_attention")
+    return out
+

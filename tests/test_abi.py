@@ -182,3 +182,26 @@ def test_delta_curve_rejects_bad_arguments(L):
     assert dc(S=0) == INVALID and dc(W=FAKE + 8) == INVALID and dc(out=FAKE + (3 << 32) + 4) == INVALID
     assert dc(ldw=700) == INVALID and dc(lds=770) == INVALID and dc(stride=100) == INVALID
     assert L.lpv_last_error().decode() != ""
+
+
+def test_encoder_calls_reject_bad_arguments(L):
+    # every check runs before any HIP call; empty batches return OK untouched
+    ln = lambda x=FAKE, y=0, M=10, D=768, dt=2, g=FAKE + (1 << 32), b=FAKE + (2 << 32), eps=1e-6, \
+        S=0, out=FAKE + (3 << 32): L.lpv_add_layernorm(x, y, M, D, dt, g, b, ctypes.c_double(eps),
+                                                       S, out, None)
+    assert ln(dt=0) == DTYPE and ln(dt=9) == DTYPE
+    assert ln(D=2) == SHAPE and ln(D=770) == SHAPE and ln(D=4096) == SHAPE
+    assert ln(M=-1) == SHAPE and ln(M=1 << 31) == SHAPE
+    assert ln(eps=-1.0) == INVALID and ln(eps=float("inf")) == INVALID
+    assert ln(g=0) == INVALID and ln(b=FAKE + 4) == INVALID and ln(x=0) == INVALID
+    assert ln(out=FAKE + 2) == INVALID and ln(y=FAKE + 6) == INVALID and ln(S=FAKE + 4) == INVALID
+    assert ln(M=0, x=0, out=0) == OK
+    at = lambda q=FAKE, n=4, T=197, H=12, hd=64, dt=2, out=FAKE + (1 << 32): \
+        L.lpv_attention(q, n, T, H, hd, dt, out, None)
+    assert at(dt=0) == DTYPE and at(hd=32) == SHAPE and at(hd=128) == SHAPE
+    assert at(T=0) == SHAPE and at(T=513) == SHAPE and at(H=0) == SHAPE and at(H=65) == SHAPE
+    assert at(n=-1) == SHAPE and at(n=1 << 24) == SHAPE
+    assert at(q=0) == INVALID and at(out=FAKE + 8) == INVALID
+    assert at(out=FAKE + 64) == ALIAS
+    assert at(n=0, q=0, out=0) == OK
+    assert L.lpv_last_error().decode() != ""
