@@ -407,54 +407,82 @@ def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
 
 
 def time_stack(steps, to_dev):
-    """The DeiT-B linear stack at batch 256: 12 layers of qkv -> proj -> fc1 +
-    GELU -> fc2, each at its own sparsity (uniform in [30, 80]%, Zipf-skewed
-    rows), chained on the GPU (proj reads the V third of qkv in place).  Kept
-    TFLOP/s of the whole chain, beside the same chain through the library's
-    dense kernel."""
+    """The DeiT-B encoder at batch 256 (256 x 197 tokens): 12 pre-norm blocks of
+    LN -> qkv -> multi-head attention (12 heads of 64) -> proj -> residual ->
+    LN -> fc1 + GELU -> fc2 -> residual, the four linear layers of each block
+    at their own sparsity (uniform in [30, 80]%, Zipf-skewed rows), chained on
+    the GPU; beside it the same chain with the library's dense kernel for the
+    linear layers.  LN weights are ones and zeros (seeded weights elsewhere).
+    The residual stream alternates between two buffers, so every run computes
+    the same function of the input."""
     import torch
 
     import workloads as wl
     from paper_2407_02068_amd import lpv
     layers = wl.b_stack()
-    M = layers[0].M
+    M, D, T, H = layers[0].M, 768, 197, 12
+    n_seq = M // T
     hs = [lpv.bsr_pack(to_dev(w.W), torch.from_numpy(w.mask).cuda(), w.b_r, w.b_c) for w in layers]
     Wd = [to_dev(w.W) for w in layers]
     bs = [to_dev(w.bias) for w in layers]
     X0 = to_dev(layers[0].X)
     tt = X0.dtype
-    qkv = torch.empty((M, 2304), dtype=tt, device="cuda")
-    P = torch.empty((M, 768), dtype=tt, device="cuda")
-    H = torch.empty((M, 3072), dtype=tt, device="cuda")
-    Xs = [torch.empty((M, 768), dtype=tt, device="cuda") for _ in range(2)]
+    g1 = torch.ones(D, dtype=tt, device="cuda")
+    b0 = torch.zeros(D, dtype=tt, device="cuda")
+    qkv = torch.empty((M, 3 * D), dtype=tt, device="cuda")
+    A = torch.empty((M, D), dtype=tt, device="cuda")    # normalised input of qkv / fc1
+    O = torch.empty((M, D), dtype=tt, device="cuda")    # attention output
+    P = torch.empty((M, D), dtype=tt, device="cuda")    # proj / fc2 output
+    Hh = torch.empty((M, 4 * D), dtype=tt, device="cuda")
+    R = [torch.empty((M, D), dtype=tt, device="cuda") for _ in range(2)]  # residual stream
+
+    def lin(sparse, j, x, y):
+        epi = "gelu" if layers[j].gelu else None
+        if sparse:
+            lpv.bsr_linear(hs[j], x, bs[j], y, epi=epi)
+        else:
+            lpv.dense_linear(Wd[j], x, bs[j], y, epi=epi)
 
     def chain(sparse):
-        x = X0
+        x, nxt = X0, 0
+        lpv.add_layernorm(x, None, g1, b0, 1e-6, out=A)
         for l in range(len(layers) // 4):
-            ws = range(4 * l, 4 * l + 4)
-            outs = (qkv, P, H, Xs[l % 2])
-            ins = (x, qkv[:, 1536:], P, H)
-            for i, j in enumerate(ws):
-                epi = "gelu" if layers[j].gelu else None
-                if sparse:
-                    lpv.bsr_linear(hs[j], ins[i], bs[j], outs[i], epi=epi)
-                else:
-                    lpv.dense_linear(Wd[j], ins[i], bs[j], outs[i], epi=epi)
-            x = Xs[l % 2]
+            q, pr, f1, f2 = range(4 * l, 4 * l + 4)
+            lin(sparse, q, A, qkv)
+            lpv.attention(qkv, n_seq, T, H, out=O)
+            lin(sparse, pr, O, P)
+            lpv.add_layernorm(x, P, g1, b0, 1e-6, S=R[nxt], out=A)   # x + attn; LN2
+            x, nxt = R[nxt], 1 - nxt
+            lin(sparse, f1, A, Hh)
+            lin(sparse, f2, Hh, P)
+            lpv.add_layernorm(x, P, g1, b0, 1e-6, S=R[nxt], out=A)   # x + mlp; next LN1
+            x, nxt = R[nxt], 1 - nxt
 
     n = max(5, steps // 50)
     _, sms = time_launches(lambda: chain(True), n, 3)
     _, dms = time_launches(lambda: chain(False), n, 3)
+    _, ams = time_launches(lambda: lpv.attention(qkv, n_seq, T, H, out=O), max(10, steps // 5), 5)
+    _, lms = time_launches(lambda: lpv.add_layernorm(R[0], P, g1, b0, 1e-6, S=R[1], out=A),
+                           max(10, steps // 5), 5)
     for h in hs:
         h.close()
     kept = sum(w.kept_flops() for w in layers)
     dense = sum(w.dense_flops() for w in layers)
+    att_flops = 4.0 * n_seq * H * T * T * 64          # QK^T and PV, per block
+    ln_bytes = 4.0 * M * D * 2                          # x, y read; S, out written
     avg = lambda ms: sum(ms) / len(ms)
-    return {"layers": len(layers) // 4, "linears": len(layers),
+    return {"blocks": len(layers) // 4, "linears": len(layers),
             "kept_gflop": round(kept / 1e9, 1), "dense_gflop": round(dense / 1e9, 1),
-            "ms": round(avg(sms), 4), "tflops": round(kept / (avg(sms) * 1e-3) / 1e12, 1),
+            "ms": round(avg(sms), 4), "images_per_s": round(n_seq / (avg(sms) * 1e-3), 1),
+            "linear_tflops": round(kept / (avg(sms) * 1e-3) / 1e12, 1),
             "dense_ms": round(avg(dms), 4), "speedup_vs_dense": round(avg(dms) / avg(sms), 3),
-            "note": "event averages of the whole chain; DeiT-B, 50432 tokens, 32x32 blocks"}
+            "attention_ms": round(avg(ams), 5),
+            "attention_tflops": round(att_flops / (avg(ams) * 1e-3) / 1e12, 1),
+            "add_layernorm_ms": round(avg(lms), 5),
+            "add_layernorm_GBs": round(ln_bytes / (avg(lms) * 1e-3) / 1e9, 1),
+            "note": "event averages of the whole encoder (12 blocks, 25 LN, 12 attention, 48 "
+                    "linear launches); DeiT-B, 256 x 197 tokens, 32x32 blocks; attention and LN "
+                    "timed alone at the same shape"}
 
 
 def pct(ms, q):
@@ -501,7 +529,7 @@ def main():
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the backward and delta-curve timings")
     ap.add_argument("--no-power", action="store_true", help="skip the amd-smi power leg")
-    ap.add_argument("--no-stack", action="store_true", help="skip the 12-layer DeiT-B stack")
+    ap.add_argument("--no-stack", action="store_true", help="skip the 12-block DeiT-B encoder")
     ap.add_argument("--no-flushed", action="store_true",
                     help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
@@ -625,9 +653,12 @@ def main():
     if power:
         log("power: %s" % json.dumps(power))
     if stack:
-        log("DeiT-B linear stack: %.2f ms per chain of %d linears (%.0f TFLOP/s kept), dense "
-            "%.2f ms (speedup %.2fx)" % (stack["ms"], stack["linears"], stack["tflops"],
-                                         stack["dense_ms"], stack["speedup_vs_dense"]))
+        log("DeiT-B encoder (12 blocks, batch 256): %.2f ms (%.0f images/s), dense linears "
+            "%.2f ms (speedup %.2fx); attention %.1f us (%.0f TFLOP/s), add+LN %.1f us "
+            "(%.0f GB/s)" % (stack["ms"], stack["images_per_s"], stack["dense_ms"],
+                             stack["speedup_vs_dense"], stack["attention_ms"] * 1e3,
+                             stack["attention_tflops"], stack["add_layernorm_ms"] * 1e3,
+                             stack["add_layernorm_GBs"]))
     if dcurve:
         log("delta curve: %.1f us for %d samples x %d points (%.0f GB/s of %d MB)"
             % (dcurve["ms"] * 1e3, dcurve["n_samples"], dcurve["points"],
@@ -672,7 +703,7 @@ def main():
         "backward": back,
         "delta_curve": dcurve,
         "power": power,
-        "stack": stack,
+        "encoder": stack,
         "pack_ms": round(pack_ms, 3),
         "mask_topk_ms_median": round(pct(mgms, .5), 5),
         "roofline": {"bound": "mfma", "achieved": round(achieved, 1), "peak": PEAK_BF16_TFLOPS,

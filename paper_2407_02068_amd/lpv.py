@@ -355,7 +355,7 @@ def delta_curve(W, grad, samples, b_r, b_c, kappa, pcts, out=None, stream=None):
     return out
 
 
-def _vec(t, name, dtype, n):
+def _param(t, name, dtype, n):
     if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != dtype or t.numel() != n \
             or not t.is_contiguous():
         raise ValueError("%s must be a contiguous %s GPU tensor of %d elements" % (name, dtype, n))
@@ -375,7 +375,7 @@ def add_layernorm(x, y, gamma, beta, eps, S=None, out=None, stream=None):
             raise ValueError("%s must be a contiguous tensor shaped and typed like x" % n)
     ptr = lambda t: ctypes.c_void_p(t.data_ptr() if t is not None else 0)
     _check(lib().lpv_add_layernorm(ptr(x), ptr(y), M, D, DTYPES[x.dtype],
-                                   _vec(gamma, "gamma", x.dtype, D), _vec(beta, "beta", x.dtype, D),
+                                   _param(gamma, "gamma", x.dtype, D), _param(beta, "beta", x.dtype, D),
                                    float(eps), ptr(S), ptr(out), _stream(stream)),
            "lpv_add_layernorm")
     return out
