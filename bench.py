@@ -6,9 +6,13 @@ uniformly at random (exactly 1152 of 2304), no GELU.
 
 A step is one lpv_bsr_linear call over the whole batch (X staging, kept-block
 contraction, epilogue); the weight is packed once before timing (weights are
-static at inference) and the pack is timed on its own.  The dense path
-(lpv_dense_linear, same shape, same epilogue) is timed the same way for the
-speed-up.  Prints ONE JSON line on stdout; details go to stderr.
+static at inference) and the pack is timed on its own.  Before any timing the
+GPU runs block-sparse and dense launches alternately for a fixed time, so the
+clock has settled whatever --warmup is; then W untimed and K timed steps give
+`value`.  The speed-up over the dense path (lpv_dense_linear, same shape, same
+epilogue) comes from interleaved rounds (block-sparse, dense, block-sparse,
+...), so both see the same clock; the GPU clock during those rounds is sampled
+and reported.  Prints ONE JSON line on stdout; details go to stderr.
 
     python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu] [--gelu]
 """
@@ -137,29 +141,64 @@ def kernel_label(name):
 
 
 STATS_RUN = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bench -o bench --output-format csv "
-             "-- python bench.py --no-cpu --no-flushed --no-power --no-backward --no-stack")
+             "-- python bench.py --steps 20 --warmup 5 2> gpurun_out/prof_bench.log")
 STATS_RUN_BACKWARD = ("rocprofv3 --kernel-trace --stats -d gpurun_out/prof_bw -o bw --output-format "
-                      "csv -- python bench.py --no-cpu --no-flushed --no-power --no-stack")
+                      "csv -- python bench.py --no-cpu --no-flushed --no-power --no-stack --no-sweep")
 
 
-def write_stats(stats_csv, command, backward=False):
+def timed_window(trace_csv, bench_log):
+    """Durations (us) of the block-sparse launches inside bench.py's timed
+    steps, from the rocprofv3 kernel trace: the run's stderr names the window
+    (``STATS_WINDOW first=F steps=K``: the K launches after the first F of the
+    headline kernel), and the trace lists every dispatch with its start and
+    end time."""
+    import csv
+    import re
+    m = None
+    for line in open(bench_log):
+        m = re.search(r"STATS_WINDOW first=(\d+) steps=(\d+)", line) or m
+    if m is None:
+        raise SystemExit("%s: no STATS_WINDOW line" % bench_log)
+    first, steps = int(m.group(1)), int(m.group(2))
+    rows = [r for r in csv.DictReader(open(trace_csv)) if SPARSE_KERNEL in r["Kernel_Name"]]
+    rows.sort(key=lambda r: int(r["Start_Timestamp"]))
+    win = rows[first:first + steps]
+    if len(win) != steps:
+        raise SystemExit("%s: %d launches of the kernel, window %d+%d" % (trace_csv, len(rows),
+                                                                         first, steps))
+    return [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in win]
+
+
+def write_stats(stats_csv, command, backward=False, trace_csv=None, bench_log=None):
     """The rocprofv3 --kernel-trace --stats summary of a bench.py run as a
-    short table next to the other profiles: the forward run, or (backward)
-    the run with the backward and delta-curve legs."""
+    short table next to the other profiles: the run the driver makes (forward,
+    sweep, encoder, ...), or (backward) the run with the backward and
+    delta-curve legs.  For the forward run the block-sparse kernel's launches
+    inside the timed steps are averaged on their own (the stats table mixes
+    every shape the run launches the same kernel at)."""
     import csv
     rows = list(csv.DictReader(open(stats_csv)))
     text = ["# rocprofv3 kernel statistics: DeiT-B fc1 (X 50432 x 768 -> 3072), bf16, 32x32 blocks, "
             "50%% block sparsity, %s" % ("forward, backward and delta curve" if backward else
-                                         "forward"), "",
+                                         "the default bench.py run"), "",
             "Profiled run, then this summary (from the repository root on one MI355X):", "", "```",
-            STATS_RUN_BACKWARD if backward else STATS_RUN, command, "```", "",
-            "| kernel | calls | avg us | min us | max us | % of GPU time |",
-            "|---|---:|---:|---:|---:|---:|"]
+            STATS_RUN_BACKWARD if backward else STATS_RUN, command, "```", ""]
+    if not backward and trace_csv:
+        win = timed_window(trace_csv, bench_log)
+        avg_us = sum(win) / len(win)
+        text += ["Block-sparse kernel inside the %d timed steps (from the kernel trace): mean "
+                 "%.1f us, min %.1f us, max %.1f us: %.0f TFLOP/s on the 118.98 GFLOP of kept "
+                 "work (%.1f%% of the 2.5 PFLOP/s bf16 matrix-core peak).  `bench.py` times the "
+                 "same launches with HIP events on their stream and reports that mean as "
+                 "`roofline.achieved`." % (len(win), avg_us, min(win), max(win),
+                                           118.98e9 / (avg_us * 1e-6) / 1e12,
+                                           118.98e9 / (avg_us * 1e-6) / 1e12 / 25.0), ""]
+    text += ["| kernel | calls | avg us | min us | max us | % of GPU time |",
+             "|---|---:|---:|---:|---:|---:|"]
     for r in rows:
         text.append("| %s | %s | %.1f | %.1f | %.1f | %.2f |" % (
             kernel_label(r["Name"]), r["Calls"], float(r["AverageNs"]) / 1e3,
             float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3, float(r["Percentage"])))
-    sp = [r for r in rows if SPARSE_KERNEL in r["Name"]]
     if backward:
         text += ["", "The block-sparse k_linear16 row counts the forward launches and the dX "
                  "launches (the same kernel on the transposed handle).  dW is k_gradw_tiles + "
@@ -167,14 +206,10 @@ def write_stats(stats_csv, command, backward=False):
                  "k_block_scores + k_rank_counts + k_rank_scatter + k_delta_dots + "
                  "k_delta_steps + k_delta_finish; Cijk_Ailk is hipBLASLt's dense G^T X "
                  "reference, Custom_Cijk_Alik its dense forward."]
-    elif sp:
-        avg_us = float(sp[0]["AverageNs"]) / 1e3
-        text += ["", "The hipBLASLt row (Cijk) is `torch.addmm` at the same shape, a check on the "
-                 "dense path.  Kept work of one block-sparse launch: 118.98 GFLOP, so the "
-                 "block-sparse average above is %.0f TFLOP/s (%.1f%% of the 2.5 PFLOP/s bf16 "
-                 "matrix-core peak); `bench.py` times the same launches with HIP events on their "
-                 "stream and reports that average as `roofline.achieved`."
-                 % (118.98e9 / (avg_us * 1e-6) / 1e12, 118.98e9 / (avg_us * 1e-6) / 1e12 / 25.0)]
+    else:
+        text += ["", "Rows of one kernel name cover every shape the run launches it at (the "
+                 "headline, the sweep, the encoder's linears).  The hipBLASLt rows (Cijk) are "
+                 "`torch.addmm` at the headline shape, a check on the dense path."]
     with open(STATS_FILE_BACKWARD if backward else STATS_FILE, "w") as f:
         f.write("\n".join(text) + "\n")
     print("\n".join(text))
@@ -233,6 +268,113 @@ def time_launches(fn, steps, warmup):
     wall = time.perf_counter() - t0
     ms = sorted(s.elapsed_time(e) for s, e in zip(starts, ends))
     return wall, ms
+
+
+def prewarm(fns, seconds):
+    """Run the launch functions in turn until ``seconds`` have passed (the GPU
+    clock and power state settle); returns the number of calls of each."""
+    import torch
+    n = [0] * len(fns)
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for i, fn in enumerate(fns):
+            for _ in range(20):
+                fn()
+            n[i] += 20
+        torch.cuda.synchronize()
+    return n
+
+
+def interleaved(fa, fb, rounds, per_round):
+    """Rounds of ``per_round`` launches of fa, then of fb, each launch between
+    its own pair of events on the launching stream; returns (a_ms, b_ms), the
+    per-launch times of each, so both sides are measured on the same clock."""
+    import torch
+    a, b = [], []
+    for _ in range(rounds):
+        for fn, out in ((fa, a), (fb, b)):
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(per_round)]
+            for e0, e1 in ev:
+                e0.record()
+                fn()
+                e1.record()
+            torch.cuda.synchronize()
+            out.extend(e0.elapsed_time(e1) for e0, e1 in ev)
+    return a, b
+
+
+class ClockSampler:
+    """The GPU's graphics clock (MHz) sampled every 10 ms through amd-smi while
+    a block runs (``with ClockSampler() as c: ...``; then c.summary())."""
+
+    def __init__(self):
+        self.samples, self.error, self._stop, self._th, self._h = [], None, None, None, None
+
+    def _read(self):
+        import amdsmi
+        v = amdsmi.amdsmi_get_clock_info(self._h, amdsmi.AmdSmiClkType.GFX).get("clk")
+        return float(v) if isinstance(v, (int, float)) and v > 0 else None
+
+    def __enter__(self):
+        import threading
+        try:
+            import amdsmi
+            amdsmi.amdsmi_init()
+            self._h = _smi_handle(amdsmi)
+            if self._h is None:
+                raise RuntimeError("no amd-smi device matches the benchmarked GPU")
+            self._read()
+        except Exception as e:  # no amd-smi access: reported as such
+            self.error = "amdsmi: %s" % e
+            return self
+        self._stop = threading.Event()
+
+        def poll():
+            while not self._stop.is_set():
+                try:
+                    v = self._read()
+                except Exception:
+                    v = None
+                if v is not None:
+                    self.samples.append(v)
+                self._stop.wait(0.01)
+        self._th = threading.Thread(target=poll)
+        self._th.start()
+        return self
+
+    def __exit__(self, *a):
+        if self._th is not None:
+            self._stop.set()
+            self._th.join()
+        try:
+            import amdsmi
+            amdsmi.amdsmi_shut_down()
+        except Exception:
+            pass
+
+    def summary(self):
+        if not self.samples:
+            return {"unavailable": self.error or "no samples"}
+        v = sorted(self.samples)
+        return {"median_MHz": v[len(v) // 2], "min_MHz": v[0], "max_MHz": v[-1],
+                "samples": len(v), "source": "amd-smi GFX clock every 10 ms"}
+
+
+def _smi_handle(amdsmi):
+    """The amd-smi handle of the GPU torch uses (device 0)."""
+    import torch
+    handles = amdsmi.amdsmi_get_processor_handles()
+    if len(handles) == 1:
+        return handles[0]
+    p = torch.cuda.get_device_properties(0)
+    want = (getattr(p, "pci_domain_id", None), getattr(p, "pci_bus_id", None),
+            getattr(p, "pci_device_id", None))
+    for c in handles:
+        dom, bus, rest = amdsmi.amdsmi_get_gpu_device_bdf(c).split(":")
+        if (int(dom, 16), int(bus, 16), int(rest.split(".")[0], 16)) == want:
+            return c
+    return None
 
 
 def time_flushed(fn, steps, flush_buf):
@@ -315,15 +457,15 @@ def time_delta_curve(w, W, steps, to_dev):
                     "ratio steps; per-sample gradients seeded N(0, 1e-2)"}
 
 
-def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
+def measure_power(sparse, dense, seconds=1.5, settle=0.3, pairs=3, unit="launch"):
     """Board power in the manner of the paper's measurement (the power meter
     averaged over a period, idle subtracted): amd-smi's socket power sampled
-    every 20 ms during an idle period, a loop of block-sparse launches and a
-    loop of dense launches (alternating, samples of each window's first
-    ``settle`` seconds dropped).  Energy per launch above idle = (power - idle)
-    x time per launch.  Beside it, the paper's power model: the within-block
-    products scale with the kept blocks.  (amd-smi's energy counter lags the
-    windows on this machine, so it is not used.)"""
+    every 20 ms over windows of idle, a loop of block-sparse calls and a loop
+    of dense calls -- idle, then ``pairs`` x (block-sparse, dense), then idle
+    -- the samples of each window's first ``settle`` seconds dropped.  Energy
+    per call above idle = (window power - idle) x time per call, per window;
+    reported as the mean over the windows with their spread.  (amd-smi's
+    energy counter lags the windows on this machine, so it is not used.)"""
     import threading
 
     import torch
@@ -333,16 +475,7 @@ def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
     except Exception as e:  # no amd-smi access on this machine
         return {"unavailable": "amdsmi: %s" % e}
     try:
-        handles = amdsmi.amdsmi_get_processor_handles()
-        h = handles[0] if len(handles) == 1 else None
-        if h is None:
-            p = torch.cuda.get_device_properties(0)
-            want = (getattr(p, "pci_domain_id", None), getattr(p, "pci_bus_id", None),
-                    getattr(p, "pci_device_id", None))
-            for c in handles:
-                dom, bus, rest = amdsmi.amdsmi_get_gpu_device_bdf(c).split(":")
-                if (int(dom, 16), int(bus, 16), int(rest.split(".")[0], 16)) == want:
-                    h = c
+        h = _smi_handle(amdsmi)
         if h is None:
             return {"unavailable": "no amd-smi device matches the benchmarked GPU"}
 
@@ -368,9 +501,9 @@ def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
                 time.sleep(seconds)
             else:
                 while time.perf_counter() - t0 < seconds:
-                    for _ in range(50):
+                    for _ in range(10):
                         fn()
-                    n += 50
+                    n += 10
                     torch.cuda.synchronize()
             el = time.perf_counter() - t0
             stop.set()
@@ -380,23 +513,28 @@ def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
             return sum(samples) / len(samples), n, el
 
         runs = {"idle": [], "bsr": [], "dense": []}
-        for kind, fn in (("idle", None), ("bsr", sparse), ("dense", dense), ("bsr", sparse),
-                         ("dense", dense), ("idle", None)):
+        order = [("idle", None)] + [("bsr", sparse), ("dense", dense)] * pairs + [("idle", None)]
+        for kind, fn in order:
             runs[kind].append(window(fn))
+        idle = sum(r[0] for r in runs["idle"]) / len(runs["idle"])
+        # energy per call above idle, one value per window (mJ)
+        e = {k: [(wt - idle) * el / n * 1e3 for wt, n, el in runs[k]] for k in ("bsr", "dense")}
         watts = {k: sum(r[0] for r in v) / len(v) for k, v in runs.items()}
-        per_launch_s = {k: sum(r[2] for r in v) / sum(r[1] for r in v) for k, v in runs.items()
-                        if k != "idle"}
-        e = {k: (watts[k] - watts["idle"]) * per_launch_s[k] * 1e3 for k in per_launch_s}  # mJ
-        return {"idle_W": round(watts["idle"], 1), "bsr_W": round(watts["bsr"], 1),
+        mean = lambda v: sum(v) / len(v)
+        red = [100.0 * (1.0 - b / d) for b, d in zip(e["bsr"], e["dense"]) if d > 0]
+        return {"idle_W": round(idle, 1), "bsr_W": round(watts["bsr"], 1),
                 "dense_W": round(watts["dense"], 1),
-                "bsr_mJ_per_launch_above_idle": round(e["bsr"], 2),
-                "dense_mJ_per_launch_above_idle": round(e["dense"], 2),
-                "energy_reduction_pct": round(100.0 * (1.0 - e["bsr"] / e["dense"]), 1)
-                if e["dense"] > 0 else None,
-                "power_model_kept_fraction": round(w.nnzb / w.mask.size, 4),
-                "method": "amd-smi current socket power every 20 ms over %.1f s windows "
-                          "(idle, block-sparse, dense, block-sparse, dense, idle; first %.1f s "
-                          "of each dropped)" % (seconds, settle)}
+                "bsr_mJ_per_%s_above_idle" % unit: round(mean(e["bsr"]), 2),
+                "dense_mJ_per_%s_above_idle" % unit: round(mean(e["dense"]), 2),
+                "bsr_mJ_windows": [round(v, 2) for v in e["bsr"]],
+                "dense_mJ_windows": [round(v, 2) for v in e["dense"]],
+                "energy_reduction_pct": round(100.0 * (1.0 - mean(e["bsr"]) / mean(e["dense"])), 1)
+                if mean(e["dense"]) > 0 else None,
+                "energy_reduction_pct_min_max": [round(min(red), 1), round(max(red), 1)] if red else None,
+                "method": "amd-smi current socket power every 20 ms over %.1f s windows (idle, "
+                          "%d x (block-sparse, dense), idle; first %.1f s of each dropped); "
+                          "energy per %s = (window power - idle) x time per %s"
+                          % (seconds, pairs, settle, unit, unit)}
     except Exception as e:
         return {"unavailable": "amdsmi: %s" % e}
     finally:
@@ -406,83 +544,131 @@ def measure_power(sparse, dense, w, seconds=2.0, settle=0.3):
             pass
 
 
-def time_stack(steps, to_dev):
+def time_stack(steps, to_dev, power=True):
     """The DeiT-B encoder at batch 256 (256 x 197 tokens): 12 pre-norm blocks of
     LN -> qkv -> multi-head attention (12 heads of 64) -> proj -> residual ->
     LN -> fc1 + GELU -> fc2 -> residual, the four linear layers of each block
     at their own sparsity (uniform in [30, 80]%, Zipf-skewed rows), chained on
-    the GPU; beside it the same chain with the library's dense kernel for the
-    linear layers.  LN weights are ones and zeros (seeded weights elsewhere).
-    The residual stream alternates between two buffers, so every run computes
-    the same function of the input."""
+    the GPU by paper_2407_02068_amd.encoder (the composition the encoder
+    tests check link by link); beside it the same chain with the library's
+    dense kernel for the linear layers.  The linear layers' own time is the
+    sum of their launches' event times inside the chain.  With ``power``, the
+    board energy per 256 images above idle, block-sparse against dense."""
     import torch
 
     import workloads as wl
-    from paper_2407_02068_amd import lpv
+    from paper_2407_02068_amd.encoder import deit_chain
     layers = wl.b_stack()
-    M, D, T, H = layers[0].M, 768, 197, 12
-    n_seq = M // T
-    hs = [lpv.bsr_pack(to_dev(w.W), torch.from_numpy(w.mask).cuda(), w.b_r, w.b_c) for w in layers]
-    Wd = [to_dev(w.W) for w in layers]
-    bs = [to_dev(w.bias) for w in layers]
+    T, H = 197, 12
+    n_seq = layers[0].M // T
+    chain = deit_chain(layers, to_dev, n_seq, T, H)
     X0 = to_dev(layers[0].X)
-    tt = X0.dtype
-    g1 = torch.ones(D, dtype=tt, device="cuda")
-    b0 = torch.zeros(D, dtype=tt, device="cuda")
-    qkv = torch.empty((M, 3 * D), dtype=tt, device="cuda")
-    A = torch.empty((M, D), dtype=tt, device="cuda")    # normalised input of qkv / fc1
-    O = torch.empty((M, D), dtype=tt, device="cuda")    # attention output
-    P = torch.empty((M, D), dtype=tt, device="cuda")    # proj / fc2 output
-    Hh = torch.empty((M, 4 * D), dtype=tt, device="cuda")
-    R = [torch.empty((M, D), dtype=tt, device="cuda") for _ in range(2)]  # residual stream
-
-    def lin(sparse, j, x, y):
-        epi = "gelu" if layers[j].gelu else None
-        if sparse:
-            lpv.bsr_linear(hs[j], x, bs[j], y, epi=epi)
-        else:
-            lpv.dense_linear(Wd[j], x, bs[j], y, epi=epi)
-
-    def chain(sparse):
-        x, nxt = X0, 0
-        lpv.add_layernorm(x, None, g1, b0, 1e-6, out=A)
-        for l in range(len(layers) // 4):
-            q, pr, f1, f2 = range(4 * l, 4 * l + 4)
-            lin(sparse, q, A, qkv)
-            lpv.attention(qkv, n_seq, T, H, out=O)
-            lin(sparse, pr, O, P)
-            lpv.add_layernorm(x, P, g1, b0, 1e-6, S=R[nxt], out=A)   # x + attn; LN2
-            x, nxt = R[nxt], 1 - nxt
-            lin(sparse, f1, A, Hh)
-            lin(sparse, f2, Hh, P)
-            lpv.add_layernorm(x, P, g1, b0, 1e-6, S=R[nxt], out=A)   # x + mlp; next LN1
-            x, nxt = R[nxt], 1 - nxt
-
-    n = max(5, steps // 50)
-    _, sms = time_launches(lambda: chain(True), n, 3)
-    _, dms = time_launches(lambda: chain(False), n, 3)
-    _, ams = time_launches(lambda: lpv.attention(qkv, n_seq, T, H, out=O), max(10, steps // 5), 5)
+    sparse = lambda: chain.run(X0, sparse=True)
+    dense = lambda: chain.run(X0, sparse=False)
+    n = max(5, steps // 4)
+    prewarm([sparse, dense], 0.5)
+    sms, dms = interleaved(sparse, dense, 3, n)
+    ev_s, ev_d = [], []
+    for _ in range(3):  # the linear launches alone, inside the chain
+        chain.run(X0, sparse=True, linear_events=ev_s)
+        chain.run(X0, sparse=False, linear_events=ev_d)
+    torch.cuda.synchronize()
+    lin_s = sum(a.elapsed_time(b) for a, b in ev_s) / 3
+    lin_d = sum(a.elapsed_time(b) for a, b in ev_d) / 3
+    from paper_2407_02068_amd import lpv
+    A, O, qkv, R, P = chain.A, chain.O, chain.qkv, chain.R, chain.P
+    g1, b0 = chain.gamma, chain.beta
+    _, ams = time_launches(lambda: lpv.attention(qkv, n_seq, T, H, out=O), max(10, steps // 2), 5)
     _, lms = time_launches(lambda: lpv.add_layernorm(R[0], P, g1, b0, 1e-6, S=R[1], out=A),
-                           max(10, steps // 5), 5)
-    for h in hs:
-        h.close()
+                           max(10, steps // 2), 5)
+    pw = measure_power(sparse, dense, unit="256_images") if power else None
+    chain.close()
     kept = sum(w.kept_flops() for w in layers)
-    dense = sum(w.dense_flops() for w in layers)
+    dense_fl = sum(w.dense_flops() for w in layers)
     att_flops = 4.0 * n_seq * H * T * T * 64          # QK^T and PV, per block
-    ln_bytes = 4.0 * M * D * 2                          # x, y read; S, out written
+    ln_bytes = 4.0 * layers[0].M * 768 * 2              # x, y read; S, out written
     avg = lambda ms: sum(ms) / len(ms)
     return {"blocks": len(layers) // 4, "linears": len(layers),
-            "kept_gflop": round(kept / 1e9, 1), "dense_gflop": round(dense / 1e9, 1),
+            "kept_gflop": round(kept / 1e9, 1), "dense_gflop": round(dense_fl / 1e9, 1),
             "ms": round(avg(sms), 4), "images_per_s": round(n_seq / (avg(sms) * 1e-3), 1),
-            "linear_tflops": round(kept / (avg(sms) * 1e-3) / 1e12, 1),
             "dense_ms": round(avg(dms), 4), "speedup_vs_dense": round(avg(dms) / avg(sms), 3),
+            "linear_ms": round(lin_s, 4), "linear_dense_ms": round(lin_d, 4),
+            "linear_tflops": round(kept / (lin_s * 1e-3) / 1e12, 1),
+            "linear_speedup_vs_dense": round(lin_d / lin_s, 3),
             "attention_ms": round(avg(ams), 5),
             "attention_tflops": round(att_flops / (avg(ams) * 1e-3) / 1e12, 1),
             "add_layernorm_ms": round(avg(lms), 5),
             "add_layernorm_GBs": round(ln_bytes / (avg(lms) * 1e-3) / 1e9, 1),
+            "power": pw,
             "note": "event averages of the whole encoder (12 blocks, 25 LN, 12 attention, 48 "
-                    "linear launches); DeiT-B, 256 x 197 tokens, 32x32 blocks; attention and LN "
-                    "timed alone at the same shape"}
+                    "linear launches), block-sparse and dense chains interleaved; linear_ms = the "
+                    "48 linear launches' event times inside the chain (linear_tflops = kept "
+                    "FLOPs / linear_ms); DeiT-B, 256 x 197 tokens, 32x32 blocks; attention and "
+                    "LN timed alone at the same shape"}
+
+
+def sweep(steps, cfgs=("fc1", "s_fc1", "b_layer")):
+    """Every measured point besides the headline: the DeiT-B fc1 sweep (blocks
+    16/32/64 x sparsity 0/25/50/75/90% x bf16/fp16, exact-count uniform masks),
+    DeiT-S fc1 with bias + GELU (batch 64, top-half L2 masks) and the four
+    linears of one DeiT-B layer (batch 128).  Each point: block-sparse and
+    dense launches interleaved (3 rounds), kept TFLOP/s, the fraction of the
+    bf16/fp16 matrix-core peak and the speed-up over lpv_dense_linear."""
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_2407_02068_amd import lpv
+    pts = []
+
+    def todev(a, dtype):
+        a = np.ascontiguousarray(a)
+        if dtype == "bf16":
+            return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
+        return torch.from_numpy(a).cuda()
+
+    def point(w, X, cfg):
+        W, b = todev(w.W, w.dtype), todev(w.bias, w.dtype)
+        h = lpv.bsr_pack(W, torch.from_numpy(w.mask).cuda(), w.b_r, w.b_c)
+        Y = torch.empty((X.shape[0], w.N), dtype=X.dtype, device="cuda")
+        Yd = torch.empty_like(Y)
+        epi = "gelu" if w.gelu else None
+        fs = lambda: lpv.bsr_linear(h, X, b, Y, epi=epi)
+        fd = lambda: lpv.dense_linear(W, X, b, Yd, epi=epi)
+        prewarm([fs, fd], 0.05)
+        n = max(5, min(20, steps))
+        a, d = interleaved(fs, fd, 3, n)
+        h.close()
+        ts, td = pct(sorted(a), .5), pct(sorted(d), .5)
+        kept = w.kept_flops(X.shape[0])
+        pts.append({"config": cfg, "workload": w.name, "M": X.shape[0], "N": w.N, "K": w.K,
+                    "block": [w.b_r, w.b_c], "sparsity_pct": w.meta.get("sparsity"),
+                    "dtype": w.dtype, "gelu": w.gelu, "kept_gflop": round(kept / 1e9, 3),
+                    "bsr_us": round(ts * 1e3, 1), "dense_us": round(td * 1e3, 1),
+                    "tflops": round(kept / (ts * 1e-3) / 1e12, 1),
+                    "frac_of_peak": round(kept / (ts * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                    "speedup_vs_dense": round(td / ts, 3)})
+        log("sweep %-28s %7.1f us (dense %7.1f us) %6.1f TFLOP/s  x%.2f" % (
+            w.name, ts * 1e3, td * 1e3, pts[-1]["tflops"], pts[-1]["speedup_vs_dense"]))
+
+    if "fc1" in cfgs:
+        for dtype in ("bf16", "f16"):
+            X = todev(wl.activations(4, 0, 256 * 197, 768, dtype), dtype)
+            for block in wl.FC1_SWEEP_BLOCKS:
+                for sp in wl.FC1_SWEEP_SPARSITY:
+                    point(wl.b_fc1(block=block, sparsity=sp, dtype=dtype, with_x=False), X,
+                          "b_fc1_sweep")
+            del X
+    if "s_fc1" in cfgs:
+        w = wl.s_fc1_gelu()
+        point(w, todev(w.X, w.dtype), "s_fc1_gelu")
+    if "b_layer" in cfgs:
+        for w in wl.b_layer():
+            point(w, todev(w.X, w.dtype), "b_layer")
+    torch.cuda.synchronize()
+    return {"points": pts,
+            "note": "median event time of 3 interleaved rounds per point (block-sparse, dense); "
+                    "frac_of_peak against the 2.5 PFLOP/s dense bf16/fp16 matrix-core peak"}
 
 
 def pct(ms, q):
@@ -522,14 +708,18 @@ def cpu_baseline(w, target_s=12.0):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    # defaults: the clock settles within the 2000 untimed launches (~0.4 s)
-    ap.add_argument("--steps", type=int, default=500)
-    ap.add_argument("--warmup", type=int, default=2000)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--prewarm-s", type=float, default=1.5,
+                    help="seconds of alternating block-sparse and dense launches before any timing")
+    ap.add_argument("--rounds", type=int, default=8,
+                    help="interleaved block-sparse / dense rounds for the speed-up")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-backward", action="store_true",
                     help="skip the backward and delta-curve timings")
-    ap.add_argument("--no-power", action="store_true", help="skip the amd-smi power leg")
+    ap.add_argument("--no-power", action="store_true", help="skip the amd-smi power legs")
     ap.add_argument("--no-stack", action="store_true", help="skip the 12-block DeiT-B encoder")
+    ap.add_argument("--no-sweep", action="store_true", help="skip the sweep of the other configs")
     ap.add_argument("--no-flushed", action="store_true",
                     help="skip the cold-cache timing (kernel statistics of warm launches only)")
     ap.add_argument("--gelu", action="store_true", help="fused GELU epilogue (secondary point)")
@@ -540,8 +730,9 @@ def main():
                     help="only 3 launches of each path and a 1 GiB device copy (rocprofv3 counter runs)")
     ap.add_argument("--write-traffic", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="turn two --profile-pass counter CSVs into the HBM traffic summary")
-    ap.add_argument("--write-stats", metavar="STATS_CSV",
-                    help="turn a rocprofv3 --stats kernel CSV of this script into the statistics summary")
+    ap.add_argument("--write-stats", nargs=3, metavar=("STATS_CSV", "TRACE_CSV", "BENCH_LOG"),
+                    help="turn a rocprofv3 --kernel-trace --stats run of this script (its stats "
+                         "and kernel-trace CSVs and the run's stderr) into the statistics summary")
     ap.add_argument("--write-stats-backward", metavar="STATS_CSV",
                     help="the same for the run with the backward and delta-curve legs")
     ap.add_argument("--write-clock", metavar="CLOCK_CSV",
@@ -552,7 +743,8 @@ def main():
         write_traffic(*args.write_traffic, command=" ".join(["python bench.py"] + sys.argv[1:]))
         return
     if args.write_stats:
-        write_stats(args.write_stats, command=" ".join(["python bench.py"] + sys.argv[1:]))
+        write_stats(args.write_stats[0], " ".join(["python bench.py"] + sys.argv[1:]),
+                    trace_csv=args.write_stats[1], bench_log=args.write_stats[2])
         return
     if args.write_stats_backward:
         write_stats(args.write_stats_backward,
@@ -582,7 +774,7 @@ def main():
 
     def to_dev(a):
         a = np.ascontiguousarray(a)
-        if w.dtype == "bf16":
+        if a.dtype == np.uint16:
             return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).cuda()
         return torch.from_numpy(a).cuda()
 
@@ -598,7 +790,12 @@ def main():
     h = lpv.bsr_pack(W, mask, w.b_r, w.b_c)
     pack_ms = (time.perf_counter() - t0) * 1e3
 
-    sparse = lambda: lpv.bsr_linear(h, X, b, Y, epi=epi)
+    n_sparse = [0]  # launches of the block-sparse kernel at this shape so far
+
+    def sparse():
+        n_sparse[0] += 1
+        lpv.bsr_linear(h, X, b, Y, epi=epi)
+
     dense = lambda: lpv.dense_linear(W, X, b, Yd, epi=epi)
     if args.profile_pass:
         for _ in range(3):
@@ -615,15 +812,24 @@ def main():
     # the block mask of the same weight on the GPU (scores + top-k), one-time per weight
     maskgen = lambda: lpv.mask_topk(W, w.b_r, w.b_c, args.sparsity)
     _, mgms = time_launches(maskgen, 20, 3)
-    wall, ms = time_launches(sparse, args.steps, args.warmup)
-    dwall, dms = time_launches(dense, args.steps, args.warmup)
-    # torch.matmul (hipBLASLt) at the same shape, as a check on the dense path only
+    # settle the clock (independent of --warmup), then the contract's W + K steps
+    prewarm([sparse, dense], args.prewarm_s)
+    for _ in range(args.warmup):
+        sparse()
+    torch.cuda.synchronize()
+    log("STATS_WINDOW first=%d steps=%d" % (n_sparse[0], args.steps))
+    wall, ms = time_launches(sparse, args.steps, 0)
+    # the speed-up: block-sparse and dense rounds interleaved on the same clock
+    with ClockSampler() as clock:
+        ims, dms = interleaved(sparse, dense, args.rounds, max(10, args.steps // 4))
+    # torch.addmm (hipBLASLt) at the same shape, as a check on the dense path only
     bl = lambda: torch.addmm(b, X, W.t())
-    _, bms = time_launches(bl, args.steps, args.warmup)
+    _, bms = time_launches(bl, max(20, args.steps // 2), 5)
+    sw = None if args.no_sweep else sweep(args.steps)
     back = None if args.no_backward else time_backward(w, h, W, X, args.steps, tt, to_dev)
     dcurve = None if args.no_backward else time_delta_curve(w, W, args.steps, to_dev)
-    power = None if args.no_power else measure_power(sparse, dense, w)
-    stack = None if args.no_stack else time_stack(args.steps, to_dev)
+    power = None if args.no_power else measure_power(sparse, dense)
+    stack = None if args.no_stack else time_stack(args.steps, to_dev, power=not args.no_power)
     # cold caches: the same launches after a 1 GiB write each
     fms = fdms = None
     if not args.no_flushed:
@@ -641,11 +847,17 @@ def main():
     alg_bytes = algorithmic_bytes(M, N, K, w.nnzb, w.b_r, w.b_c, kused)
     hbm_gbs = alg_bytes / (ev_avg * 1e-3) / 1e9
     traffic = measured_traffic()
-    dense_avg = sum(dms) / len(dms)
-    log("bsr_linear: median %.1f us (p10 %.1f, p90 %.1f), %.0f TFLOP/s effective, %.0f GB/s alg."
-        % (pct(ms, .5) * 1e3, pct(ms, .1) * 1e3, pct(ms, .9) * 1e3, achieved, hbm_gbs))
-    log("dense_linear: median %.1f us, %.0f TFLOP/s; hipBLASLt addmm median %.1f us"
-        % (pct(dms, .5) * 1e3, w.dense_flops() / (dense_avg * 1e-3) / 1e12, pct(bms, .5) * 1e3))
+    ims, dms = sorted(ims), sorted(dms)
+    i_med, d_med = pct(ims, .5), pct(dms, .5)
+    log("bsr_linear (timed steps): mean %.1f us, median %.1f us (p10 %.1f, p90 %.1f), %.0f TFLOP/s "
+        "effective, %.0f GB/s alg." % (ev_avg * 1e3, pct(sorted(ms), .5) * 1e3,
+                                       pct(sorted(ms), .1) * 1e3, pct(sorted(ms), .9) * 1e3,
+                                       achieved, hbm_gbs))
+    log("interleaved: bsr_linear median %.1f us, dense_linear median %.1f us (%.0f TFLOP/s), "
+        "speedup %.3fx; clock %s" % (i_med * 1e3, d_med * 1e3,
+                                      w.dense_flops() / (d_med * 1e-3) / 1e12, d_med / i_med,
+                                      json.dumps(clock.summary())))
+    log("hipBLASLt addmm median %.1f us" % (pct(bms, .5) * 1e3))
     if back:
         log("backward: dX %.1f us (dense %.1f us), dW %.1f us (hipBLASLt full G^T X %.1f us), "
             "db %.1f us" % (back["dx_ms"] * 1e3, back["dx_dense_ms"] * 1e3, back["dw_ms"] * 1e3,
@@ -654,11 +866,14 @@ def main():
         log("power: %s" % json.dumps(power))
     if stack:
         log("DeiT-B encoder (12 blocks, batch 256): %.2f ms (%.0f images/s), dense linears "
-            "%.2f ms (speedup %.2fx); attention %.1f us (%.0f TFLOP/s), add+LN %.1f us "
-            "(%.0f GB/s)" % (stack["ms"], stack["images_per_s"], stack["dense_ms"],
-                             stack["speedup_vs_dense"], stack["attention_ms"] * 1e3,
-                             stack["attention_tflops"], stack["add_layernorm_ms"] * 1e3,
-                             stack["add_layernorm_GBs"]))
+            "%.2f ms (speedup %.2fx); linears alone %.2f ms vs %.2f ms (%.0f TFLOP/s); "
+            "attention %.1f us (%.0f TFLOP/s), add+LN %.1f us (%.0f GB/s)"
+            % (stack["ms"], stack["images_per_s"], stack["dense_ms"], stack["speedup_vs_dense"],
+               stack["linear_ms"], stack["linear_dense_ms"], stack["linear_tflops"],
+               stack["attention_ms"] * 1e3, stack["attention_tflops"],
+               stack["add_layernorm_ms"] * 1e3, stack["add_layernorm_GBs"]))
+        if stack.get("power"):
+            log("encoder power: %s" % json.dumps(stack["power"]))
     if dcurve:
         log("delta curve: %.1f us for %d samples x %d points (%.0f GB/s of %d MB)"
             % (dcurve["ms"] * 1e3, dcurve["n_samples"], dcurve["points"],
@@ -688,18 +903,26 @@ def main():
                                   " + GELU" if w.gelu else ", no GELU"),
                    "M": M, "N": N, "K": K, "block": [w.b_r, w.b_c], "sparsity_pct": args.sparsity,
                    "nnzb": w.nnzb, "kept_gflop": round(kept_flops / 1e9, 2)},
-        "speedup_vs_dense": round(dense_avg / ev_avg, 3),
-        "dense_ms": round(dense_avg, 5),
-        "bsr_ms_median": round(pct(ms, .5), 5),
-        "bsr_ms_p10": round(pct(ms, .1), 5),
-        "bsr_ms_p90": round(pct(ms, .9), 5),
+        "speedup_vs_dense": round(d_med / i_med, 3),
+        "interleaved": {"rounds": args.rounds, "per_round": max(10, args.steps // 4),
+                        "bsr_ms_median": round(i_med, 5), "bsr_ms_p10": round(pct(ims, .1), 5),
+                        "bsr_ms_p90": round(pct(ims, .9), 5),
+                        "dense_ms_median": round(d_med, 5), "dense_ms_p10": round(pct(dms, .1), 5),
+                        "dense_ms_p90": round(pct(dms, .9), 5),
+                        "dense_tflops": round(w.dense_flops() / (d_med * 1e-3) / 1e12, 1),
+                        "gpu_clock": clock.summary()},
+        "prewarm_s": args.prewarm_s,
+        "bsr_ms_median": round(pct(sorted(ms), .5), 5),
+        "bsr_ms_p10": round(pct(sorted(ms), .1), 5),
+        "bsr_ms_p90": round(pct(sorted(ms), .9), 5),
         "hipblaslt_addmm_ms": round(pct(bms, .5), 5),
-        "speedup_vs_hipblaslt": round(pct(bms, .5) / pct(ms, .5), 3),
+        "speedup_vs_hipblaslt": round(pct(bms, .5) / i_med, 3),
         "flushed": None if not fms else {
             "bsr_ms_median": round(pct(fms, .5), 5), "bsr_ms_p90": round(pct(fms, .9), 5),
             "dense_ms_median": round(pct(fdms, .5), 5),
             "speedup_vs_dense": round(pct(fdms, .5) / pct(fms, .5), 3),
             "note": "each launch after a 1 GiB device write (L2 and MALL evicted)"},
+        "sweep": sw,
         "backward": back,
         "delta_curve": dcurve,
         "power": power,
@@ -710,6 +933,8 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
                      "traffic": traffic,
                      "kernel": "k_linear16 (lpv_bsr_linear)",
+                     "achieved_from": "kept FLOPs / mean HIP-event duration of the %d timed steps"
+                                      % args.steps,
                      "hbm_alg_bytes": alg_bytes, "hbm_achieved_GBs": round(hbm_gbs, 1),
                      "hbm_peak_GBs": PEAK_HBM_GBS, "hbm_frac": round(hbm_gbs / PEAK_HBM_GBS, 4)},
     }

@@ -356,12 +356,53 @@ def block_mask(W, dtype, b_r, b_c, sparsity_pct, G=None):
 
 
 def rel_err(y, ref):
-    """Infinity-norm relative error ``max|y - r| / max|r|`` (float64); when the
-    reference is all zero, 0.0 if ``y`` is exactly zero too, else inf."""
+    """Infinity-norm relative error ``max|y - r| / max|r|`` (float64), the
+    reading of "max relative error" used for every value check.  The scale is
+    the reference's largest magnitude, never the result's.  When the reference
+    is all zero (or empty), 0.0 if ``y`` is exactly zero there too, else inf.
+    A non-finite ``y`` anywhere, or a shape mismatch, gives inf: the check
+    ``rel_err(y, r) <= tol`` then fails."""
     y = np.asarray(y, np.float64)
     ref = np.asarray(ref, np.float64)
-    scale = np.max(np.abs(ref)) if ref.size else 0.0
-    diff = np.max(np.abs(y - ref)) if ref.size else 0.0
+    if y.shape != ref.shape or not np.all(np.isfinite(y)):
+        return float("inf")
+    if ref.size == 0:
+        return 0.0
+    scale = float(np.max(np.abs(ref)))
+    diff = float(np.max(np.abs(y - ref)))
     if scale == 0.0:
         return 0.0 if diff == 0.0 else float("inf")
-    return float(diff / scale)
+    return diff / scale
+
+
+def rel_err_tiles(y, ref, tile_rows=32, tile_cols=32):
+    """The same measure taken per output tile: the largest, over every
+    ``tile_rows x tile_cols`` tile of the 2-D result (ragged tiles at the
+    edges included), of ``max|y - r| / max|r|`` within the tile.  An error
+    confined to small-magnitude rows or to one tile (a wrong bias, a dropped
+    block) then shows even when the whole result's maximum is far larger.
+    Same conventions as rel_err: a tile whose reference is all zero must be
+    exactly zero; non-finite values or a shape mismatch give inf."""
+    y = np.asarray(y, np.float64)
+    ref = np.asarray(ref, np.float64)
+    if y.shape != ref.shape or not np.all(np.isfinite(y)):
+        return float("inf")
+    if ref.ndim == 1:
+        y, ref = y[None, :], ref[None, :]
+    if ref.ndim != 2:
+        raise ValueError("rel_err_tiles takes 1-D or 2-D results")
+    M, N = ref.shape
+    if M == 0 or N == 0:
+        return 0.0
+    pm, pn = -M % tile_rows, -N % tile_cols
+    # zero padding changes neither a tile's largest difference nor its scale
+    d = np.pad(np.abs(y - ref), ((0, pm), (0, pn)))
+    a = np.pad(np.abs(ref), ((0, pm), (0, pn)))
+    shape = ((M + pm) // tile_rows, tile_rows, (N + pn) // tile_cols, tile_cols)
+    diff = d.reshape(shape).max(axis=(1, 3))
+    scale = a.reshape(shape).max(axis=(1, 3))
+    if np.any((scale == 0.0) & (diff != 0.0)):
+        return float("inf")
+    nz = scale > 0.0
+    return float(np.max(diff[nz] / scale[nz])) if np.any(nz) else 0.0
+    return worst

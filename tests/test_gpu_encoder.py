@@ -6,9 +6,10 @@ import torch
 
 import oracle
 import workloads as wl
-from gpu_util import TOL, dev, f64, say
+from gpu_util import TOL, assert_close, dev, f64, host, say
 from oracle import encoder as enc
 from paper_2407_02068_amd import lpv
+from paper_2407_02068_amd.encoder import deit_chain
 
 pytestmark = pytest.mark.gpu
 
@@ -16,7 +17,7 @@ T_QKV, T_LNX, T_LNY, T_LNG = 40, 41, 42, 43
 
 
 def rel(y, ref):
-    return np.abs(y - ref).max() / max(np.abs(ref).max(), 1e-30)
+    return oracle.rel_err(y, ref)
 
 
 def gen(cfg, tid, shape, dtype, std=1.0, mean=0.0):
@@ -124,3 +125,63 @@ def test_add_layernorm_deit_b_batch_sampled():
     rows = np.array([0, 1, 12345, M // 2, M - 1])
     _, o_ref = enc.add_layernorm(x[rows], y[rows], g, b, 1e-6)
     assert rel(f64(out)[rows], o_ref) <= TOL["bf16"]
+
+
+# ---- the chained encoder (the composition bench.py times) -----------------------
+
+def _check_chain(n_seq, blocks, seqs):
+    """Run the DeiT-B encoder chain (block-sparse linears with the stack's
+    Zipf masks and per-linear sparsity) and check every link on the token rows
+    of sequences ``seqs`` against the oracle fed the GPU's own input of that
+    link: the linear layers with oracle.linear, attention and residual + layer
+    norm with the encoder oracle."""
+    T, H, D = 197, 12, 768
+    layers = wl.b_stack(M=n_seq * T, layers=blocks)
+    chain = deit_chain(layers, lambda a: dev(a, "bf16"), n_seq, T, H)
+    by_name = {w.name: w for w in layers}
+    rows = np.concatenate([np.arange(s * T, (s + 1) * T) for s in seqs])
+    rd = torch.from_numpy(rows).cuda()
+    ones, zeros = np.ones(D), np.zeros(D)
+    seen = []
+
+    def dec(t):  # the GPU tensor's sampled rows, decoded exactly to float64
+        return oracle.decode(host(t[rd].contiguous(), "bf16"), "bf16").reshape(len(rows), -1)
+
+    def trace(name, ins, out):
+        torch.cuda.synchronize()
+        seen.append(name)
+        if name in by_name:
+            w = by_name[name]
+            xin = host(ins["x"][rd].contiguous(), "bf16")
+            r = oracle.linear(xin, w.W, "bf16", 32, 32, w.mask, w.bias, gelu=w.gelu)
+            assert_close(f64(out[rd]), r, "bf16", name)
+        elif name.endswith("attention"):
+            r = enc.attention(dec(ins["qkv"]), len(seqs), T, H, 64)
+            assert_close(f64(out[rd]), r, "bf16", name)
+        else:
+            y = dec(ins["y"]) if "y" in ins else None
+            s_ref, o_ref = enc.add_layernorm(dec(ins["x"]), y, ones, zeros, 1e-6)
+            if "s" in ins:
+                assert_close(f64(ins["s"][rd]), s_ref, "bf16", name + " residual")
+            assert_close(f64(out[rd]), o_ref, "bf16", name)
+
+    say("encoder chain", n_seq, "sequences,", blocks, "blocks, checked on", list(seqs))
+    x0 = dev(layers[0].X, "bf16")
+    x, A = chain.run(x0, sparse=True, trace=trace)
+    torch.cuda.synchronize()
+    assert len(seen) == 1 + 7 * blocks
+    assert torch.isfinite(A.float()).all()
+    # the dense-linear chain computes the same function of the same weights
+    # with every block of the masks kept: here only its finiteness and shape
+    x2, A2 = chain.run(x0, sparse=False)
+    torch.cuda.synchronize()
+    assert torch.isfinite(A2.float()).all() and A2.shape == A.shape
+    chain.close()
+
+
+def test_encoder_chain_batch4_in_full():
+    _check_chain(4, 2, range(4))
+
+
+def test_encoder_chain_batch256_sampled():
+    _check_chain(256, 1, (0, 77, 255))
