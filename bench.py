@@ -113,9 +113,15 @@ def write_traffic(fetch_csv, write_csv, command):
 
 def kernel_label(name):
     """A short name for a kernel of the rocprofv3 statistics."""
-    labels = ((SPARSE_KERNEL, "k_linear16 bf16 block-sparse (lpv_bsr_linear)"),
-              (DENSE_KERNEL, "k_linear16 bf16 dense (lpv_dense_linear)"),
-              ("k_block_scores<2, true", "k_block_scores, Taylor (lpv_delta_curve)"),
+    import re
+    m = re.search(r"k_linear16<(\d), (true|false), (true|false), (true|false)>", name)
+    if m:
+        return "k_linear16 %s %s%s%s (%s)" % (
+            {"2": "bf16", "1": "fp16"}[m.group(1)],
+            "dense" if m.group(3) == "true" else "block-sparse",
+            " + GELU" if m.group(2) == "true" else "", ", K tail" if m.group(4) == "true" else "",
+            "lpv_dense_linear" if m.group(3) == "true" else "lpv_bsr_linear")
+    labels = (("k_block_scores<2, true", "k_block_scores, Taylor (lpv_delta_curve)"),
               ("k_block_scores<2, false", "k_block_scores, sum of squares (lpv_mask_topk)"),
               ("k_block_scores", "k_block_scores (lpv_mask_topk)"),
               ("k_delta_dots", "k_delta_dots (lpv_delta_curve)"),
@@ -124,7 +130,11 @@ def kernel_label(name):
               ("k_delta_steps", "k_delta_steps (lpv_delta_curve)"),
               ("k_delta_finish", "k_delta_finish (lpv_delta_curve)"),
               ("k_mask_topk", "k_mask_topk (lpv_mask_topk)"),
-              ("FillFunctor", "torch fill (cache flush between cold launches)"))
+              ("k_attention", "k_attention (lpv_attention)"),
+              ("k_add_layernorm", "k_add_layernorm (lpv_add_layernorm)"),
+              ("FillFunctor", "torch fill (cache flush between cold launches)"),
+              ("copyBuffer", "HIP runtime copy"),
+              ("direct_copy_kernel", "torch copy"))
     for key, label in labels:
         if key in name:
             return label
@@ -137,6 +147,8 @@ def kernel_label(name):
                      ("k_unpack", "lpv_bsr_unpack")):
         if key in name:
             return "%s (%s)" % (key, api)
+    if name.startswith("Cijk") or name.startswith("Custom_Cijk"):
+        return "hipBLASLt " + name.split("_UserArgs")[0][:48]
     return name.split("(")[0][:72]
 
 
@@ -211,6 +223,80 @@ def write_stats(stats_csv, command, backward=False, trace_csv=None, bench_log=No
                  "headline, the sweep, the encoder's linears).  The hipBLASLt rows (Cijk) are "
                  "`torch.addmm` at the headline shape, a check on the dense path."]
     with open(STATS_FILE_BACKWARD if backward else STATS_FILE, "w") as f:
+        f.write("\n".join(text) + "\n")
+    print("\n".join(text))
+
+
+COUNTER_FILE = os.path.join(ROOT, "profiles", "bsr_linear_fc1_counters.md")
+COUNTER_PASSES = (
+    "SQ_WAVE_CYCLES SQ_BUSY_CYCLES SQ_WAIT_ANY SQ_WAIT_INST_ANY SQ_ACTIVE_INST_ANY "
+    "SQ_ACTIVE_INST_LDS SQ_INSTS_LDS SQ_LDS_BANK_CONFLICT",
+    "SQ_VALU_MFMA_BUSY_CYCLES SQ_WAIT_INST_LDS SQ_LDS_IDX_ACTIVE SQ_INSTS_MFMA SQ_INSTS_SALU "
+    "SQ_INSTS_VALU SQ_INSTS_VMEM SQ_WAVES GRBM_GUI_ACTIVE",
+    "TCC_HIT_sum TCC_MISS_sum GRBM_GUI_ACTIVE")
+
+
+def write_counters(csvs, command):
+    """Derived figures of the block-sparse (and dense) kernel from three
+    rocprofv3 --pmc passes of ``--profile-pass`` (COUNTER_PASSES, one CSV per
+    pass): matrix-core busy share, wave-cycle shares waiting / issuing, LDS
+    activity and bank conflicts, L2 hit rate.  Counter values are summed over
+    the device by rocprofv3; GRBM_GUI_ACTIVE is summed over the XCDs."""
+    import csv
+    vals = {}
+    n_xcc = 8
+    for path in csvs:
+        agents = os.path.join(os.path.dirname(path),
+                              os.path.basename(path).replace("counter_collection", "agent_info"))
+        try:
+            n_xcc = max(int(a.get("Num_Xcc") or 0) for a in csv.DictReader(open(agents))) or n_xcc
+        except (OSError, ValueError):
+            pass
+        for r in csv.DictReader(open(path)):
+            for key, tag in ((SPARSE_KERNEL, "bsr"), (DENSE_KERNEL, "dense")):
+                if key in r["Kernel_Name"]:
+                    vals.setdefault((tag, r["Counter_Name"]), []).append(float(r["Counter_Value"]))
+    avg = {k: sum(v) / len(v) for k, v in vals.items()}
+
+    def derived(tag):
+        g = lambda c: avg.get((tag, c))
+        cyc = g("GRBM_GUI_ACTIVE") / n_xcc  # cycles of the dispatch, per XCD
+        cus, simds = 256, 1024
+        out = [("dispatch cycles (GRBM_GUI_ACTIVE per XCD)", "%.0f" % cyc),
+               ("matrix cores busy (SQ_VALU_MFMA_BUSY_CYCLES / (cycles x %d SIMDs))" % simds,
+                "%.1f%%" % (100 * g("SQ_VALU_MFMA_BUSY_CYCLES") / (cyc * simds))),
+               ("wave cycles waiting on anything (SQ_WAIT_ANY / SQ_WAVE_CYCLES)",
+                "%.1f%%" % (100 * g("SQ_WAIT_ANY") / g("SQ_WAVE_CYCLES"))),
+               ("wave cycles waiting on a dependency, s_waitcnt (SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES)",
+                "%.1f%%" % (100 * g("SQ_WAIT_INST_ANY") / g("SQ_WAVE_CYCLES"))),
+               ("wave cycles issuing (SQ_ACTIVE_INST_ANY / SQ_WAVE_CYCLES)",
+                "%.1f%%" % (100 * g("SQ_ACTIVE_INST_ANY") / g("SQ_WAVE_CYCLES"))),
+               ("LDS busy (SQ_LDS_IDX_ACTIVE / (cycles x %d CUs))" % cus,
+                "%.1f%%" % (100 * g("SQ_LDS_IDX_ACTIVE") / (cyc * cus))),
+               ("LDS bank-conflict cycles / LDS active cycles",
+                "%.2f%%" % (100 * g("SQ_LDS_BANK_CONFLICT") / g("SQ_LDS_IDX_ACTIVE"))),
+               ("instructions per wave: MFMA / SALU / VALU / LDS / VMEM", "%.0f / %.0f / %.0f / %.0f / %.0f" % (
+                   g("SQ_INSTS_MFMA") / g("SQ_WAVES"), g("SQ_INSTS_SALU") / g("SQ_WAVES"),
+                   g("SQ_INSTS_VALU") / g("SQ_WAVES"), g("SQ_INSTS_LDS") / g("SQ_WAVES"),
+                   g("SQ_INSTS_VMEM") / g("SQ_WAVES"))),
+               ("L2 hit rate (TCC_HIT / (TCC_HIT + TCC_MISS))",
+                "%.1f%%" % (100 * g("TCC_HIT_sum") / (g("TCC_HIT_sum") + g("TCC_MISS_sum"))))]
+        return out
+
+    text = ["# rocprofv3 counters: DeiT-B fc1 (X 50432 x 768 -> 3072), bf16, 32x32 blocks, "
+            "50% block sparsity", "",
+            "Three counter passes over `bench.py --profile-pass` (three launches of each path), "
+            "then this summary (from the repository root on one MI355X):", "", "```"]
+    for i, c in enumerate(COUNTER_PASSES):
+        text.append("rocprofv3 --pmc %s -d gpurun_out/pmc_c%d -o c%d --output-format csv -- "
+                    "python bench.py --profile-pass" % (c, i + 1, i + 1))
+    text += [command, "```", "",
+             "| figure | k_linear16 block-sparse | k_linear16 dense |", "|---|---:|---:|"]
+    for (name, a), (_, b) in zip(derived("bsr"), derived("dense")):
+        text.append("| %s | %s | %s |" % (name, a, b))
+    text += ["", "Counter values are per dispatch, averaged over the three launches; SQ counters "
+             "are summed over the device, GRBM_GUI_ACTIVE over the %d XCDs." % n_xcc]
+    with open(COUNTER_FILE, "w") as f:
         f.write("\n".join(text) + "\n")
     print("\n".join(text))
 
@@ -457,12 +543,14 @@ def time_delta_curve(w, W, steps, to_dev):
                     "ratio steps; per-sample gradients seeded N(0, 1e-2)"}
 
 
-def measure_power(sparse, dense, seconds=1.5, settle=0.3, pairs=3, unit="launch"):
+def measure_power(sparse, dense, seconds=2.0, settle=0.6, pairs=3, unit="launch"):
     """Board power in the manner of the paper's measurement (the power meter
     averaged over a period, idle subtracted): amd-smi's socket power sampled
     every 20 ms over windows of idle, a loop of block-sparse calls and a loop
-    of dense calls -- idle, then ``pairs`` x (block-sparse, dense), then idle
-    -- the samples of each window's first ``settle`` seconds dropped.  Energy
+    of dense calls -- idle, one block-sparse window that only brings the board
+    from idle to load (discarded: the meter's average lags), then ``pairs`` x
+    (block-sparse, dense), then idle -- the samples of each window's first
+    ``settle`` seconds dropped.  Energy
     per call above idle = (window power - idle) x time per call, per window;
     reported as the mean over the windows with their spread.  (amd-smi's
     energy counter lags the windows on this machine, so it is not used.)"""
@@ -512,10 +600,12 @@ def measure_power(sparse, dense, seconds=1.5, settle=0.3, pairs=3, unit="launch"
                 raise RuntimeError("no power samples")
             return sum(samples) / len(samples), n, el
 
-        runs = {"idle": [], "bsr": [], "dense": []}
-        order = [("idle", None)] + [("bsr", sparse), ("dense", dense)] * pairs + [("idle", None)]
+        runs = {"idle": [], "bsr": [], "dense": [], "ramp": []}
+        order = [("idle", None), ("ramp", sparse)] + [("bsr", sparse), ("dense", dense)] * pairs \
+            + [("idle", None)]
         for kind, fn in order:
             runs[kind].append(window(fn))
+        del runs["ramp"]
         idle = sum(r[0] for r in runs["idle"]) / len(runs["idle"])
         # energy per call above idle, one value per window (mJ)
         e = {k: [(wt - idle) * el / n * 1e3 for wt, n, el in runs[k]] for k in ("bsr", "dense")}
@@ -531,8 +621,9 @@ def measure_power(sparse, dense, seconds=1.5, settle=0.3, pairs=3, unit="launch"
                 "energy_reduction_pct": round(100.0 * (1.0 - mean(e["bsr"]) / mean(e["dense"])), 1)
                 if mean(e["dense"]) > 0 else None,
                 "energy_reduction_pct_min_max": [round(min(red), 1), round(max(red), 1)] if red else None,
-                "method": "amd-smi current socket power every 20 ms over %.1f s windows (idle, "
-                          "%d x (block-sparse, dense), idle; first %.1f s of each dropped); "
+                "method": "amd-smi current socket power every 20 ms over %.1f s windows (idle, a "
+                          "discarded block-sparse ramp window, %d x (block-sparse, dense), idle; "
+                          "first %.1f s of each dropped); "
                           "energy per %s = (window power - idle) x time per %s"
                           % (seconds, pairs, settle, unit, unit)}
     except Exception as e:
@@ -735,6 +826,9 @@ def main():
                          "and kernel-trace CSVs and the run's stderr) into the statistics summary")
     ap.add_argument("--write-stats-backward", metavar="STATS_CSV",
                     help="the same for the run with the backward and delta-curve legs")
+    ap.add_argument("--write-counters", nargs=3, metavar="PASS_CSV",
+                    help="turn the three --profile-pass counter CSVs (COUNTER_PASSES) into the "
+                         "counter summary")
     ap.add_argument("--write-clock", metavar="CLOCK_CSV",
                     help="turn a --profile-pass GRBM_GUI_ACTIVE counter CSV into the clock summary")
     args = ap.parse_args()
@@ -752,6 +846,9 @@ def main():
         return
     if args.write_clock:
         write_clock(args.write_clock, command=" ".join(["python bench.py"] + sys.argv[1:]))
+        return
+    if args.write_counters:
+        write_counters(args.write_counters, command=" ".join(["python bench.py"] + sys.argv[1:]))
         return
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:

@@ -16,15 +16,17 @@ ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = [
-    "-std=c++17", "-O3", "--offload-arch=" + ARCH, "-fPIC", "-shared",
+    "-std=c++17", "-O3", "--offload-arch=" + ARCH, "-fPIC",
     "-Wall", "-Wno-unused-function",
     # keep the compiler from forming packed fp32 instructions
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # matrix-core accumulators in ordinary VGPRs: the kept-tile walk branches
-    # around each tile's instructions, and accumulators in AGPRs would then be
-    # copied across every branch
-    "-mllvm", "-amdgpu-mfma-vgpr-form=1",
 ]
+# Per-source flags.  The matrix-core kernels keep their accumulators in
+# ordinary VGPRs: they branch around each tile's instructions, and at their
+# register counts accumulators in AGPRs would be copied across every branch.
+_VGPR_MFMA = ["-mllvm", "-amdgpu-mfma-vgpr-form=1"]
+SOURCE_FLAGS = {"linear.hip": _VGPR_MFMA, "backward.hip": _VGPR_MFMA, "encoder.hip": _VGPR_MFMA}
+BUILD_DIR = os.path.join(HERE, "_build")
 
 
 # Kernels whose LDS ring counts every vector-memory instruction a wave issues
@@ -48,25 +50,42 @@ def check_resources(remarks):
 
 
 def build(verbose: bool = False, extra=()) -> str:
-    srcs = [os.path.join(CSRC, s) for s in SOURCES]
+    """Compile every source to an object (in parallel), then link the shared
+    library; resource remarks are checked per object."""
+    from concurrent.futures import ThreadPoolExecutor
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    noise = "'-packed-fp32-ops' is not a recognized feature for this target"
+
+    def compile_one(src):
+        obj = os.path.join(BUILD_DIR, src.replace(".hip", ".o"))
+        cmd = ([HIPCC] + FLAGS + SOURCE_FLAGS.get(src, []) +
+               ["-Rpass-analysis=kernel-resource-usage", "-fno-caret-diagnostics"] + list(extra) +
+               ["-c", os.path.join(CSRC, src), "-o", obj])
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        p = subprocess.run(cmd, capture_output=True, text=True)
+        lines = [l for l in (p.stdout + p.stderr).splitlines() if noise not in l]
+        return src, obj, p.returncode, lines
+
+    with ThreadPoolExecutor(max_workers=min(8, len(SOURCES))) as ex:
+        results = list(ex.map(compile_one, SOURCES))
+    bad = []
+    for src, obj, rc, lines in results:
+        msgs = [l for l in lines if "remark:" not in l]
+        if rc != 0:
+            raise RuntimeError("hipcc failed on %s (%d):\n%s" % (src, rc, "\n".join(msgs)))
+        bad += check_resources([l for l in lines if "remark:" in l])
+        if verbose and msgs:
+            print("\n".join(msgs))
+    if bad:
+        raise RuntimeError("register spills in ring kernels:\n" + "\n".join(bad))
     tmp = LIB + ".tmp%d" % os.getpid()
-    cmd = [HIPCC] + FLAGS + ["-Rpass-analysis=kernel-resource-usage", "-fno-caret-diagnostics"] + list(extra) + srcs + ["-o", tmp]
+    cmd = [HIPCC, "--offload-arch=" + ARCH, "-shared", "-fPIC"] + [r[1] for r in results] + ["-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     p = subprocess.run(cmd, capture_output=True, text=True)
-    # the host pass does not know the packed-fp32 target feature and says so
-    noise = "'-packed-fp32-ops' is not a recognized feature for this target"
-    lines = [l for l in (p.stdout + p.stderr).splitlines() if noise not in l]
-    remarks = [l for l in lines if "remark:" in l]
-    msgs = [l for l in lines if "remark:" not in l]
     if p.returncode != 0:
-        raise RuntimeError("hipcc failed (%d):\n%s" % (p.returncode, "\n".join(msgs)))
-    bad = check_resources(remarks)
-    if bad:
-        os.unlink(tmp)
-        raise RuntimeError("register spills in ring kernels:\n" + "\n".join(bad))
-    if verbose and msgs:
-        print("\n".join(msgs))
+        raise RuntimeError("link failed (%d):\n%s" % (p.returncode, p.stdout + p.stderr))
     os.replace(tmp, LIB)
     return LIB
 
