@@ -255,6 +255,23 @@ lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_d
                          void* db, void* stream);
 
 /*
+ * lpv_bias_grad_noalloc -- lpv_bias_grad for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving or training
+ * loops, harnesses that forbid hipMalloc).  Same arguments, checks and result
+ * as lpv_bias_grad (the token chunking may differ, so the float32 sums may
+ * round differently, within the same bound); it calls no allocation routine.
+ * Its partial sums live in a fixed scratch array of 2^20 float32 (4 MiB) that
+ * each device the call runs on holds until the process ends; the chunk count
+ * is capped so that chunks x N fits (N up to 2^20; SHAPE above).  Every call
+ * on one device shares that array: calls that overlap in time on one device
+ * (different streams, threads) race and are not allowed.  Nothing in the
+ * array needs clearing between calls: each call writes every partial it reads.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, HIP.
+ */
+lpv_status lpv_bias_grad_noalloc(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
+                                 void* db, void* stream);
+
+/*
  * lpv_delta_curve -- the delta curve of one layer (Sec. 3.3): the second-order
  * Taylor term of pruning it at ratio alpha,
  *   delta(alpha) = grad . dW + 1/2 dW^T H dW,  H = kappa I + (1/n) sum_s g_s g_s^T

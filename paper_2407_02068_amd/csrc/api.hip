@@ -520,8 +520,11 @@ lpv_status lpv_bsr_grad_w(const lpv_bsr* h, const void* G, int64_t ldg, const vo
     return e == hipSuccess ? LPV_OK : hip_fail(e, "grad_w launch");
 }
 
-lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
-                         void* db, void* stream)
+namespace {
+
+// Shared checks of the two bias-gradient calls.
+lpv_status check_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
+                           void* db)
 {
     const int es = elem_size(dt);
     if (!es)
@@ -537,10 +540,34 @@ lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_d
         return fail(LPV_ERR_INVALID_ARG, "db must be non-NULL and aligned to its element size");
     if (M > 0 && (!G || !aligned16(G)))
         return fail(LPV_ERR_INVALID_ARG, "G must be non-NULL and 16-byte aligned");
+    return LPV_OK;
+}
+
+}  // namespace
+
+lpv_status lpv_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
+                         void* db, void* stream)
+{
+    const lpv_status st = check_bias_grad(G, ldg, M, N, dt, db);
+    if (st != LPV_OK)
+        return st;
     hipError_t e = lpv::launch_bias_grad(G, ldg, M, N, dt, db, (hipStream_t)stream);
     if (e == hipErrorOutOfMemory)
         return fail(LPV_ERR_ALLOC, "workspace allocation failed");
     return e == hipSuccess ? LPV_OK : hip_fail(e, "bias_grad launch");
+}
+
+lpv_status lpv_bias_grad_noalloc(const void* G, int64_t ldg, int64_t M, int64_t N, lpv_dtype dt,
+                                 void* db, void* stream)
+{
+    const lpv_status st = check_bias_grad(G, ldg, M, N, dt, db);
+    if (st != LPV_OK)
+        return st;
+    if (N > lpv::BIAS_NOALLOC_SCRATCH_FLOATS)
+        return fail(LPV_ERR_SHAPE, "N = %lld is above the %lld columns the fixed scratch holds",
+                    (long long)N, (long long)lpv::BIAS_NOALLOC_SCRATCH_FLOATS);
+    const hipError_t e = lpv::launch_bias_grad_noalloc(G, ldg, M, N, dt, db, (hipStream_t)stream);
+    return e == hipSuccess ? LPV_OK : hip_fail(e, "bias_grad_noalloc launch");
 }
 
 lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,

@@ -11,6 +11,8 @@
 //                     and k_gradw_reduce, or k_gradw_plain for fp32 handles
 //   db = sum_m G[m]   k_bias_partial + k_bias_reduce
 // Every sum is taken in a fixed order, so results do not depend on timing.
+#include <mutex>
+
 #include "lpv_device.h"
 #include "lpv_internal.h"
 
@@ -488,21 +490,34 @@ hipError_t launch_transpose_blocks(const lpv_bsr* h, void* WT, int64_t ldwt, uin
     return hipGetLastError();
 }
 
-hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype, void* db,
-                            hipStream_t s)
+namespace {
+
+// Token chunks of the bias gradient: about 512 workgroups (two per compute
+// unit), at least 64 rows each, and at most max_chunks.
+int64_t bias_chunks(int64_t M, int64_t N, int V, int64_t max_chunks, int64_t* rows)
+{
+    // (64-bit comparisons written out: the host min/max overloads of the HIP
+    // headers may narrow to int)
+    const int64_t bx = (N + 256 * V - 1) / (256 * V);
+    int64_t n_chunks = (512 + bx - 1) / bx;
+    if (n_chunks > max_chunks)
+        n_chunks = max_chunks;
+    if (n_chunks > (M + 63) / 64)
+        n_chunks = (M + 63) / 64;
+    if (n_chunks < 1)
+        n_chunks = 1;
+    *rows = (M + n_chunks - 1) / n_chunks;
+    return M > 0 ? (M + *rows - 1) / *rows : 0;
+}
+
+// The two kernels of the bias gradient with the partial sums in `part`
+// (n_chunks x N floats, every entry written before it is read).
+hipError_t bias_grad_kernels(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype,
+                             void* db, float* part, int64_t n_chunks, int64_t rows, hipStream_t s)
 {
     const int V = dtype == LPV_F32 ? 4 : 8;
     const int64_t bx = (N + 256 * V - 1) / (256 * V);
-    // about 512 workgroups (two per compute unit), at least 64 rows each
-    int64_t n_chunks = (512 + bx - 1) / bx;
-    n_chunks = max((int64_t)1, min(n_chunks, (M + 63) / 64));
-    const int64_t rows = (M + n_chunks - 1) / n_chunks;
-    n_chunks = M > 0 ? (M + rows - 1) / rows : 1;
-    float* part = nullptr;
-    hipError_t e = hipMallocAsync((void**)&part, (size_t)(n_chunks * N) * sizeof(float), s);
-    if (e != hipSuccess)
-        return e;
-    if (M > 0) {
+    if (n_chunks > 0) {
 #define LPV_BIAS(DT_)                                                                            \
     hipLaunchKernelGGL(k_bias_partial<DT_>, dim3((unsigned)bx, (unsigned)n_chunks), dim3(256), 0, \
                        s, (const char*)G, ldg, M, N, rows, part)
@@ -513,22 +528,68 @@ hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, in
         else
             LPV_BIAS(LPV_F32);
 #undef LPV_BIAS
-    } else {
-        n_chunks = 0;  // no tokens: db = 0
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess)
+            return e;
     }
-    e = hipGetLastError();
-    if (e == hipSuccess) {
-        const dim3 grid((unsigned)((N + 31) / 32));
-        if (dtype == LPV_BF16)
-            hipLaunchKernelGGL(k_bias_reduce<LPV_BF16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
-        else if (dtype == LPV_F16)
-            hipLaunchKernelGGL(k_bias_reduce<LPV_F16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
-        else
-            hipLaunchKernelGGL(k_bias_reduce<LPV_F32>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
-        e = hipGetLastError();
-    }
+    const dim3 grid((unsigned)((N + 31) / 32));
+    if (dtype == LPV_BF16)
+        hipLaunchKernelGGL(k_bias_reduce<LPV_BF16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
+    else if (dtype == LPV_F16)
+        hipLaunchKernelGGL(k_bias_reduce<LPV_F16>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
+    else
+        hipLaunchKernelGGL(k_bias_reduce<LPV_F32>, grid, dim3(256), 0, s, part, (int)n_chunks, N, (char*)db);
+    return hipGetLastError();
+}
+
+// Scratch of lpv_bias_grad_noalloc: the partial sums live in this file-scope
+// device array instead of an allocation.  Host code never uses the array's
+// name as an address: each device's address comes from hipGetSymbolAddress
+// on that device's first call and is kept in scratch_ptr.
+static __device__ __align__(256) float scratch[BIAS_NOALLOC_SCRATCH_FLOATS];
+
+constexpr int MAX_DEVICES = 64;
+float* scratch_ptr[MAX_DEVICES];
+std::once_flag scratch_once[MAX_DEVICES];
+hipError_t scratch_err[MAX_DEVICES];
+
+}  // namespace
+
+hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype, void* db,
+                            hipStream_t s)
+{
+    int64_t rows = 0;
+    const int64_t n_chunks = bias_chunks(M, N, dtype == LPV_F32 ? 4 : 8, (int64_t)1 << 40, &rows);
+    float* part = nullptr;
+    hipError_t e = hipMallocAsync((void**)&part, (size_t)(max(n_chunks, (int64_t)1) * N) * sizeof(float), s);
+    if (e != hipSuccess)
+        return e;
+    e = bias_grad_kernels(G, ldg, M, N, dtype, db, part, n_chunks, rows, s);
     const hipError_t ef = hipFreeAsync(part, s);
     return e != hipSuccess ? e : ef;
+}
+
+hipError_t launch_bias_grad_noalloc(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype,
+                                    void* db, hipStream_t s)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess)
+        return e;
+    if (dev < 0 || dev >= MAX_DEVICES)
+        return hipErrorInvalidDevice;
+    // once per device, with that device current (it is: hipGetDevice above)
+    std::call_once(scratch_once[dev], [dev]() {
+        void* p = nullptr;
+        scratch_err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        scratch_ptr[dev] = scratch_err[dev] == hipSuccess ? (float*)p : nullptr;
+    });
+    if (scratch_err[dev] != hipSuccess)
+        return scratch_err[dev];
+    int64_t rows = 0;
+    const int64_t n_chunks = bias_chunks(M, N, dtype == LPV_F32 ? 4 : 8,
+                                         BIAS_NOALLOC_SCRATCH_FLOATS / N, &rows);
+    return bias_grad_kernels(G, ldg, M, N, dtype, db, scratch_ptr[dev], n_chunks, rows, s);
 }
 
 hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)

@@ -137,5 +137,10 @@ hipError_t launch_attention(const void* qkv, int64_t n_seq, int32_t T, int32_t H
                             void* out, hipStream_t s);
 hipError_t launch_bias_grad(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype, void* db,
                             hipStream_t s);
+// The same with the partial sums in a fixed device array of this many floats
+// (4 MiB per device, held until the process ends): no allocation.
+constexpr int64_t BIAS_NOALLOC_SCRATCH_FLOATS = (int64_t)1 << 20;
+hipError_t launch_bias_grad_noalloc(const void* G, int64_t ldg, int64_t M, int64_t N, int dtype,
+                                    void* db, hipStream_t s);
 
 }  // namespace lpv

@@ -21,8 +21,9 @@ DTYPES = {torch.float32: 0, torch.float16: 1, torch.bfloat16: 2}
 EPI = {None: 0, "none": 0, "gelu": 1}
 EXPORTED = ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
             "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
-            "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_delta_curve",
-            "lpv_add_layernorm", "lpv_attention", "lpv_bsr_destroy", "lpv_status_str", "lpv_last_error")
+            "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_bias_grad_noalloc",
+            "lpv_delta_curve", "lpv_add_layernorm", "lpv_attention", "lpv_bsr_destroy",
+            "lpv_status_str", "lpv_last_error")
 
 
 class LpvError(RuntimeError):
@@ -67,13 +68,15 @@ def lib():
     L.lpv_bsr_transpose.argtypes = [vp, vp, ctypes.POINTER(vp)]
     L.lpv_bsr_grad_w.argtypes = [vp, vp, i64, vp, i64, i64, vp, vp]
     L.lpv_bias_grad.argtypes = [vp, i64, i64, i64, i32, vp, vp]
+    L.lpv_bias_grad_noalloc.argtypes = [vp, i64, i64, i64, i32, vp, vp]
     L.lpv_add_layernorm.argtypes = [vp, vp, i64, i64, i32, vp, vp, ctypes.c_double, vp, vp, vp]
     L.lpv_attention.argtypes = [vp, i64, i32, i32, i32, i32, vp, vp]
     L.lpv_delta_curve.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, vp, i64, i64, i64,
                                   ctypes.c_double, vp, i32, vp, vp]
     for f in ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
               "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
-              "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_delta_curve"):
+              "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_bias_grad_noalloc",
+              "lpv_delta_curve"):
         getattr(L, f).restype = i32
     L.lpv_bsr_destroy.argtypes = [vp]
     L.lpv_bsr_destroy.restype = None
@@ -326,6 +329,20 @@ def bias_grad(G, out=None, stream=None):
         raise ValueError("out must be a contiguous %s tensor of %d elements" % (G.dtype, N))
     _check(lib().lpv_bias_grad(gp, ldg, M, N, DTYPES[G.dtype], ctypes.c_void_p(out.data_ptr()),
                                _stream(stream)), "lpv_bias_grad")
+    return out
+
+
+def bias_grad_noalloc(G, out, stream=None):
+    """lpv_bias_grad_noalloc: the column sums of G (M x N) into ``out`` (N
+    elements of G's dtype, caller-allocated), with no allocation inside the
+    library (a fixed per-device scratch; overlapping calls on one GPU race)."""
+    gp, ldg = _mat(G, "G")
+    M, N = G.shape
+    if out is None or out.dtype != G.dtype or out.numel() != N or not out.is_contiguous():
+        raise ValueError("out must be a contiguous %s tensor of %d elements" % (G.dtype, N))
+    _check(lib().lpv_bias_grad_noalloc(gp, ldg, M, N, DTYPES[G.dtype],
+                                       ctypes.c_void_p(out.data_ptr()), _stream(stream)),
+           "lpv_bias_grad_noalloc")
     return out
 
 

@@ -160,6 +160,16 @@ def test_backward_rejects_bad_arguments(L):
     assert bg(db=0) == INVALID and bg(db=FAKE + 1) == INVALID
     assert bg(G=0) == INVALID and bg(G=FAKE + 8) == INVALID
     assert L.lpv_last_error().decode() != ""
+    # the no-allocation variant runs the same checks before any HIP call
+    bn = lambda G=FAKE, ldg=3072, M=10, N=3072, dt=2, db=FAKE + (1 << 32): \
+        L.lpv_bias_grad_noalloc(G, ldg, M, N, dt, db, None)
+    assert bn(dt=7) == DTYPE
+    assert bn(N=0) == SHAPE and bn(N=1 << 17) == SHAPE
+    assert bn(M=-1) == SHAPE and bn(M=1 << 31) == SHAPE
+    assert bn(ldg=3000) == INVALID and bn(ldg=3076) == INVALID
+    assert bn(db=0) == INVALID and bn(db=FAKE + 1) == INVALID
+    assert bn(G=0) == INVALID and bn(G=FAKE + 8) == INVALID
+    assert L.lpv_last_error().decode() != ""
 
 
 def test_delta_curve_rejects_bad_arguments(L):
