@@ -502,7 +502,8 @@ def time_backward(w, h, W, X, steps, tt, to_dev):
     _, xdms = time_launches(lambda: lpv.dense_linear(WT, G, None, dXd), steps, 10)
     _, wms = time_launches(lambda: lpv.grad_w(h, G, X, dW), steps, 10)
     _, wbms = time_launches(lambda: torch.mm(Gt, X), steps, 5)
-    _, bms = time_launches(lambda: lpv.bias_grad(G, db), steps, 10)
+    _, bms = time_launches(lambda: lpv.bias_grad_noalloc(G, db), steps, 10)
+    _, bams = time_launches(lambda: lpv.bias_grad(G, db), steps, 10)
     ht.close()
     kept = w.kept_flops()
     avg = lambda ms: sum(ms) / len(ms)
@@ -511,8 +512,11 @@ def time_backward(w, h, W, X, steps, tt, to_dev):
             "dw_ms": round(avg(wms), 5), "dw_tflops": round(kept / (avg(wms) * 1e-3) / 1e12, 1),
             "dw_frac_of_peak": round(kept / (avg(wms) * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
             "dw_hipblaslt_dense_ms": round(avg(wbms), 5), "db_ms": round(avg(bms), 5),
-            "note": "event averages; dW includes its stream-ordered workspace and chunk "
-                    "reduction; G seeded N(0, 1)"}
+            "db_stream_alloc_ms": round(avg(bams), 5),
+            "note": "event averages; dW includes its chunk reduction (the workspace is the "
+                    "handle's, allocated once); db by the call that allocates nothing, "
+                    "db_stream_alloc_ms by the one with a stream-ordered workspace; "
+                    "G seeded N(0, 1)"}
 
 
 def time_delta_curve(w, W, steps, to_dev):
@@ -532,15 +536,18 @@ def time_delta_curve(w, W, steps, to_dev):
         S[i] = to_dev(wl.quantize(g.normal(0, 1e-2, (w.N, w.K)).astype(np.float32), w.dtype))
     pcts = list(range(0, 101, 5))
     out = torch.empty(len(pcts), dtype=torch.float64, device="cuda")
-    _, ms = time_launches(lambda: lpv.delta_curve(W, grad, S, w.b_r, w.b_c, 1e-4, pcts, out),
-                          max(10, steps // 2), 5)
+    ws = torch.empty(lpv.delta_curve_workspace_size(w.N, w.K, w.b_r, w.b_c, n_s, len(pcts)),
+                     dtype=torch.uint8, device="cuda")
+    _, ms = time_launches(lambda: lpv.delta_curve(W, grad, S, w.b_r, w.b_c, 1e-4, pcts, out,
+                                                  workspace=ws), max(10, steps // 2), 5)
     avg = sum(ms) / len(ms)
     alg = (n_s + 2) * w.N * w.K * 2  # every vector (samples, grad, W) read once
     return {"ms": round(avg, 5), "n_samples": n_s, "points": len(pcts),
             "hbm_alg_bytes": alg, "hbm_achieved_GBs": round(alg / (avg * 1e-3) / 1e9, 1),
             "hbm_frac": round(alg / (avg * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "note": "event average; block scores, ranking, float64 block dot products and the "
-                    "ratio steps; per-sample gradients seeded N(0, 1e-2)"}
+                    "ratio steps, in a caller-owned workspace; per-sample gradients seeded "
+                    "N(0, 1e-2)"}
 
 
 def measure_power(sparse, dense, seconds=2.0, settle=0.6, pairs=3, unit="launch"):

@@ -110,12 +110,14 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
                         int32_t b_r, int32_t b_c, const uint8_t* mask, void* stream,
                         lpv_bsr** out);
 
-/* Shape, kept count and schedule sizes of a handle (host struct). */
+/* Shape, kept count and schedule sizes of a handle (host struct).  nnzb is the
+ * kept-block count of Sec. 3.4 (ceil((1 - alpha) R C) for a top-k mask). */
 lpv_status lpv_bsr_info_get(const lpv_bsr* h, lpv_bsr_info* out);
 
 /*
- * lpv_bsr_export -- copy the canonical BSR arrays (described at lpv_bsr_pack)
- * into caller device buffers: row_ptr int32[R + 1], col_idx int32[nnzb],
+ * lpv_bsr_export -- copy the canonical BSR arrays (described at lpv_bsr_pack):
+ * the kept blocks of the masked weight of Sec. 3.1, by block row, into caller
+ * device buffers: row_ptr int32[R + 1], col_idx int32[nnzb],
  * values [nnzb][b_r][b_c] of the handle's element type.  Any of the three may
  * be NULL to skip it.  Asynchronous on `stream`.
  */
@@ -124,7 +126,9 @@ lpv_status lpv_bsr_export(const lpv_bsr* h, int32_t* row_ptr, int32_t* col_idx, 
 
 /*
  * lpv_bsr_schedule_export -- copy the tile schedule into caller device buffers
- * (each may be NULL):
+ * (each may be NULL).  The schedule counts the work of each output group in
+ * kept tiles, the unit of the cost model of Sec. 3.4 (token tiles times kept
+ * blocks):
  *   group_order int32[n_groups]      groups in launch order (most work first);
  *   step_ptr    int32[n_groups + 1]  steps of group g are [step_ptr[g], step_ptr[g+1]);
  *   step_col    int32[n_steps]       tile column of each step, ascending per group;
@@ -141,8 +145,9 @@ lpv_status lpv_bsr_schedule_export(const lpv_bsr* h, int32_t* group_order, int32
                                    void* stream);
 
 /*
- * lpv_bsr_unpack -- the pruned dense weight W~ (N x K, row stride ldw >= K) into
- * a caller device buffer; dropped blocks become +0.0.  Asynchronous.
+ * lpv_bsr_unpack -- the pruned dense weight W~ = W (.) M of Sec. 3.1 (N x K,
+ * row stride ldw >= K) into a caller device buffer; dropped blocks become
+ * +0.0.  Asynchronous.
  */
 lpv_status lpv_bsr_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, void* stream);
 
@@ -155,8 +160,9 @@ lpv_status lpv_bsr_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, void* stre
  * Y     device, M x N, row stride ldy >= N; must not overlap X.
  * epi   LPV_EPI_NONE or LPV_EPI_GELU (exact-erf GELU after the bias).
  *
- * Each token tile times each group of output tile rows walks only the kept
- * tiles of its rows, on the matrix cores for bf16/fp16.  M = 0 is a no-op.
+ * The product of the input with the block-sparse weight of Sec. 3.4: each
+ * token tile times each group of output tile rows walks only the kept tiles
+ * of its rows, on the matrix cores for bf16/fp16.  M = 0 is a no-op.
  * One kernel launch per run of output groups whose per-launch tables fit in
  * LDS (a single launch for ViT-sized layers), no allocation, no host
  * synchronisation.
@@ -169,7 +175,8 @@ lpv_status lpv_bsr_linear(const lpv_bsr* h, const void* X, int64_t ldx, int64_t 
 /*
  * lpv_dense_linear -- Y = g(X * W^T + b) with a dense W (N x K, row stride
  * K <= ldw <= 2^22), through the library's own matrix-core kernel: the
- * reference point for the speed-up of the block-sparse path.  Same
+ * unpruned layer, the counterpart of the "Dense" rows of Tab. 2 and Tab. 4,
+ * and the reference point for the speed-up of the block-sparse path.  Same
  * conventions as lpv_bsr_linear; N and K must be multiples of 16.
  */
 lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
@@ -234,11 +241,15 @@ lpv_status lpv_bsr_transpose(const lpv_bsr* h, void* stream, lpv_bsr** out);
  *         columns ascending, each block row-major).
  * Sums run in float32 over fixed token chunks added in a fixed order, one
  * rounding at the end.  16-bit types use the matrix cores; fp32 handles a
- * plain kernel.  Allocates and frees a stream-ordered workspace (partial sums
- * of the kept tiles per token chunk).  M = 0 writes zeros.  G, X 16-byte
- * aligned, ldg and ldx multiples of 16 bytes and at most 2^22 elements,
- * M < 2^31.  No host synchronisation.
- * Errors: INVALID_ARG, SHAPE, ALLOC, HIP.
+ * plain kernel.  The partial sums of the kept tiles per token chunk live in a
+ * workspace the handle owns: allocated on the handle's first 16-bit call
+ * (chunks x kept tiles x 4 KiB, the chunk count fixed per handle by the
+ * device's compute-unit count) and freed by lpv_bsr_destroy, so later calls
+ * allocate nothing.  Calls on one handle that overlap in time (different
+ * streams) race on it and are not allowed; calls in one stream's order are
+ * fine.  M = 0 writes zeros.  G, X 16-byte aligned, ldg and ldx multiples of
+ * 16 bytes and at most 2^22 elements, M < 2^31.  No host synchronisation.
+ * Errors: INVALID_ARG, SHAPE, ALLOC (first call only), HIP.
  */
 lpv_status lpv_bsr_grad_w(const lpv_bsr* h, const void* G, int64_t ldg, const void* X,
                           int64_t ldx, int64_t M, void* dW, void* stream);
@@ -301,6 +312,37 @@ lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv
                            const void* samples, int64_t lds, int64_t sample_stride,
                            int64_t n_samples, double kappa, const int32_t* pcts, int32_t n_points,
                            double* delta, void* stream);
+
+/*
+ * lpv_delta_curve_ws -- lpv_delta_curve with a workspace the caller owns, for
+ * the same curve (Sec. 3.3) computed over and over (one call per layer and
+ * calibration batch) without an allocation per call.  Same arguments, checks
+ * and result as lpv_delta_curve, plus:
+ * workspace        device, at least the bytes lpv_delta_curve_workspace_size
+ *                  gives for the same shape, 16-byte aligned, non-NULL; owned
+ *                  by the caller, who must not reuse it before the call's work
+ *                  on the stream has finished.  Its contents need no clearing.
+ * workspace_bytes  its size; too small is INVALID_ARG.
+ * Allocates nothing.
+ * Errors: INVALID_ARG, SHAPE, DTYPE, BLOCK, HIP.
+ */
+lpv_status lpv_delta_curve_ws(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                              int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
+                              const void* samples, int64_t lds, int64_t sample_stride,
+                              int64_t n_samples, double kappa, const int32_t* pcts,
+                              int32_t n_points, double* delta, void* workspace,
+                              size_t workspace_bytes, void* stream);
+
+/*
+ * lpv_delta_curve_workspace_size -- the workspace lpv_delta_curve_ws needs for
+ * an N x K weight in b_r x b_c blocks, n_samples per-sample gradients and
+ * n_points sparsity points (float64 block scores and dot products, the rank
+ * tables).  Host only; writes *bytes.
+ * Errors: INVALID_ARG (NULL bytes, n_samples or n_points out of range), BLOCK,
+ * SHAPE.
+ */
+lpv_status lpv_delta_curve_workspace_size(int64_t N, int64_t K, int32_t b_r, int32_t b_c,
+                                          int64_t n_samples, int32_t n_points, size_t* bytes);
 
 /* Release a handle and its device buffers.  NULL-safe.  The caller must make
  * sure no enqueued work still uses it. */

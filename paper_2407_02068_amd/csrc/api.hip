@@ -11,6 +11,7 @@
 #include <cmath>
 #include <new>
 
+#include <mutex>
 #include "lpv_internal.h"
 
 namespace {
@@ -107,7 +108,7 @@ void free_handle(lpv_bsr* h)
     if (!h)
         return;
     void* bufs[] = {h->meta, h->col_idx, h->values, h->step_col, h->step_bits, h->step_tile,
-                    h->walk, h->stream_vals};
+                    h->walk, h->stream_vals, h->gradw_ws};
     for (void* p : bufs)
         if (p)
             (void)hipFree(p);
@@ -513,7 +514,31 @@ lpv_status lpv_bsr_grad_w(const lpv_bsr* h, const void* G, int64_t ldg, const vo
     if (dev != h->device)
         return fail(LPV_ERR_INVALID_ARG, "handle lives on device %d, current device is %d",
                     h->device, dev);
-    lpv::GradWCall c = {G, ldg, X, ldx, M, dW};
+    // the handle's workspace, allocated on its first weight-gradient call
+    // (its size does not depend on M)
+    const size_t need = lpv::grad_w_workspace_bytes(h);
+    if (M > 0 && need > h->gradw_ws_bytes) {
+        static std::mutex ws_mutex;
+        std::lock_guard<std::mutex> lock(ws_mutex);
+        if (need > h->gradw_ws_bytes) {
+            if (h->gradw_ws) {
+                e = hipDeviceSynchronize();  // (the size is fixed per handle: not reached)
+                if (e != hipSuccess)
+                    return hip_fail(e, "hipDeviceSynchronize");
+                (void)hipFree(h->gradw_ws);
+                h->gradw_ws = nullptr;
+                h->gradw_ws_bytes = 0;
+            }
+            void* p = nullptr;
+            e = dmalloc(&p, need);
+            if (e != hipSuccess)
+                return e == hipErrorOutOfMemory ? fail(LPV_ERR_ALLOC, "workspace allocation failed")
+                                                : hip_fail(e, "hipMalloc");
+            h->gradw_ws = p;
+            h->gradw_ws_bytes = need;
+        }
+    }
+    lpv::GradWCall c = {G, ldg, X, ldx, M, dW, (float*)h->gradw_ws};
     e = lpv::launch_grad_w(h, c, (hipStream_t)stream);
     if (e == hipErrorOutOfMemory)
         return fail(LPV_ERR_ALLOC, "workspace allocation failed");
@@ -570,11 +595,16 @@ lpv_status lpv_bias_grad_noalloc(const void* G, int64_t ldg, int64_t M, int64_t 
     return e == hipSuccess ? LPV_OK : hip_fail(e, "bias_grad_noalloc launch");
 }
 
-lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
-                           int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
-                           const void* samples, int64_t lds, int64_t sample_stride,
-                           int64_t n_samples, double kappa, const int32_t* pcts, int32_t n_points,
-                           double* delta, void* stream)
+}  // extern "C"
+
+namespace {
+
+lpv_status delta_curve_impl(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                            int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
+                            const void* samples, int64_t lds, int64_t sample_stride,
+                            int64_t n_samples, double kappa, const int32_t* pcts,
+                            int32_t n_points, double* delta, void* ws, size_t ws_bytes,
+                            void* stream)
 {
     g_err[0] = 0;
     const int es = elem_size(dt);
@@ -634,10 +664,64 @@ lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv
     for (int i = 0; i < n_points; ++i)
         c.keep[i] = (int32_t)(((100 - (int64_t)pcts[i]) * nb + 99) / 100);
     c.delta = delta;
+    if (ws) {
+        const size_t need = lpv::delta_workspace_bytes(N, K, b_r, b_c, n_samples, n_points);
+        if (ws_bytes < need || (uintptr_t)ws % 16)
+            return fail(LPV_ERR_INVALID_ARG, "workspace: %zu bytes 16-byte aligned are needed",
+                        need);
+    }
+    c.ws = ws;
+    c.ws_bytes = ws_bytes;
     hipError_t e = lpv::launch_delta_curve(c, (hipStream_t)stream);
     if (e == hipErrorOutOfMemory)
         return fail(LPV_ERR_ALLOC, "workspace allocation failed");
     return e == hipSuccess ? LPV_OK : hip_fail(e, "delta_curve launch");
+}
+
+}  // namespace
+
+extern "C" {
+
+lpv_status lpv_delta_curve(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                           int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
+                           const void* samples, int64_t lds, int64_t sample_stride,
+                           int64_t n_samples, double kappa, const int32_t* pcts, int32_t n_points,
+                           double* delta, void* stream)
+{
+    return delta_curve_impl(W, ldw, N, K, dt, b_r, b_c, grad, ldg, samples, lds, sample_stride,
+                            n_samples, kappa, pcts, n_points, delta, nullptr, 0, stream);
+}
+
+lpv_status lpv_delta_curve_ws(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
+                              int32_t b_r, int32_t b_c, const void* grad, int64_t ldg,
+                              const void* samples, int64_t lds, int64_t sample_stride,
+                              int64_t n_samples, double kappa, const int32_t* pcts,
+                              int32_t n_points, double* delta, void* workspace,
+                              size_t workspace_bytes, void* stream)
+{
+    if (!workspace)
+        return fail(LPV_ERR_INVALID_ARG, "workspace must not be NULL");
+    return delta_curve_impl(W, ldw, N, K, dt, b_r, b_c, grad, ldg, samples, lds, sample_stride,
+                            n_samples, kappa, pcts, n_points, delta, workspace, workspace_bytes,
+                            stream);
+}
+
+lpv_status lpv_delta_curve_workspace_size(int64_t N, int64_t K, int32_t b_r, int32_t b_c,
+                                          int64_t n_samples, int32_t n_points, size_t* bytes)
+{
+    if (!bytes)
+        return fail(LPV_ERR_INVALID_ARG, "bytes must not be NULL");
+    if (check_block(b_r) || check_block(b_c))
+        return fail(LPV_ERR_BLOCK, "block %dx%d: each side must be 16, 32 or 64", b_r, b_c);
+    if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM || N % b_r || K % b_c ||
+        (N / b_r) * (K / b_c) > lpv::DELTA_MAX_BLOCKS)
+        return fail(LPV_ERR_SHAPE, "weight %lldx%lld with %dx%d blocks", (long long)N,
+                    (long long)K, b_r, b_c);
+    if (n_samples < 0 || n_samples > 65000 || n_points < 1 || n_points > lpv::DELTA_MAX_POINTS)
+        return fail(LPV_ERR_INVALID_ARG, "n_samples in [0, 65000], n_points in [1, %d]",
+                    lpv::DELTA_MAX_POINTS);
+    *bytes = lpv::delta_workspace_bytes(N, K, b_r, b_c, n_samples, n_points);
+    return LPV_OK;
 }
 
 void lpv_bsr_destroy(lpv_bsr* h)

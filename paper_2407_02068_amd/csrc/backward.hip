@@ -592,6 +592,22 @@ hipError_t launch_bias_grad_noalloc(const void* G, int64_t ldg, int64_t M, int64
     return bias_grad_kernels(G, ldg, M, N, dtype, db, scratch_ptr[dev], n_chunks, rows, s);
 }
 
+// Token chunks of the weight gradient: about one workgroup per compute unit
+// over the (group, 8-column window) pairs, at most ceil(M / GW_TOK).
+static int64_t grad_w_chunk_cap(const lpv_bsr* h)
+{
+    const int64_t n_win = (int64_t)h->n_groups * ((h->n_tile_cols + 7) / 8);
+    return max((int64_t)1, (int64_t)device_cus() / n_win);
+}
+
+size_t grad_w_workspace_bytes(const lpv_bsr* h)
+{
+    if (h->dtype == LPV_F32 || h->nnzb == 0)
+        return 0;
+    return (size_t)(grad_w_chunk_cap(h) * (int64_t)h->n_tile_rows * h->n_tile_cols * 1024) *
+           sizeof(float);
+}
+
 hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
 {
     if (h->nnzb == 0)
@@ -620,15 +636,15 @@ hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
     d.n_wcols = (h->n_tile_cols + 7) / 8;
     const int64_t n_win = (int64_t)d.n_groups * d.n_wcols;
     // about one workgroup per compute unit; chunks of whole 32-token steps
-    int64_t n_chunks = max((int64_t)1, (int64_t)device_cus() / n_win);
+    int64_t n_chunks = grad_w_chunk_cap(h);
     n_chunks = min(n_chunks, (c.M + GW_TOK - 1) / GW_TOK);
     d.chunk_rows = ((c.M + n_chunks - 1) / n_chunks + GW_TOK - 1) / GW_TOK * GW_TOK;
     d.n_chunks = (int32_t)((c.M + d.chunk_rows - 1) / d.chunk_rows);
     const int64_t chunk_stride = (int64_t)d.n_tile_rows * d.n_tile_cols * 1024;
-    float* ws = nullptr;
-    hipError_t e = hipMallocAsync((void**)&ws, (size_t)(d.n_chunks * chunk_stride) * sizeof(float), s);
-    if (e != hipSuccess)
-        return e;
+    float* ws = c.ws;  // the handle's workspace: n_chunks <= grad_w_chunk_cap(h)
+    if (!ws)
+        return hipErrorInvalidValue;
+    hipError_t e = hipSuccess;
     d.per_xcd = (int32_t)((n_win * d.n_chunks + 7) / 8);
     const dim3 grid((unsigned)(8 * d.per_xcd)), block(GW_NT);
     const dim3 rgrid((unsigned)((total + 255) / 256));
@@ -653,8 +669,7 @@ hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
     }
     if (e == hipSuccess)
         e = hipGetLastError();
-    const hipError_t ef = hipFreeAsync(ws, s);
-    return e != hipSuccess ? e : ef;
+    return e;
 }
 
 }  // namespace lpv

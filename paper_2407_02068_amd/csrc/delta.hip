@@ -205,22 +205,39 @@ __global__ __launch_bounds__(1024) void k_delta_finish(const DeltaCall c, double
 
 }  // namespace
 
+// Ranking: keys in chunks of at least 128, at most 64 chunks.
+static int32_t rank_chunk(int64_t nb) { return (int32_t)max((int64_t)128, (nb + 63) / 64); }
+
+size_t delta_workspace_bytes(int64_t N, int64_t K, int32_t b_r, int32_t b_c, int64_t n_samples,
+                             int32_t n_points)
+{
+    const int64_t nb = (N / b_r) * (K / b_c), nv = n_samples + 2;
+    const int32_t chunk = rank_chunk(nb);
+    const int32_t n_chunks = (int32_t)((nb + chunk - 1) / chunk);
+    // scores (nb), dots (nv x nb), step sums (points x nv), step terms
+    // (points), perm (nb), rank counts (n_chunks x nb)
+    return (size_t)(nb + nv * nb + (int64_t)n_points * nv + n_points) * sizeof(double) +
+           (size_t)(nb + (int64_t)n_chunks * nb) * sizeof(int32_t);
+}
+
 hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
 {
     const int32_t R = (int32_t)(c.N / c.b_r), C = (int32_t)(c.K / c.b_c);
     const int64_t nb = (int64_t)R * C, nv = c.n_samples + 2;
-    // ranking: keys in chunks of at least 128, at most 64 chunks
-    const int32_t chunk = (int32_t)max((int64_t)128, (nb + 63) / 64);
+    const int32_t chunk = rank_chunk(nb);
     const int32_t n_chunks = (int32_t)((nb + chunk - 1) / chunk);
-    // workspace: scores (nb), dots (nv x nb), step sums (points x nv), step
-    // terms (points), perm (nb), rank counts (n_chunks x nb)
-    const size_t bytes =
-        (size_t)(nb + nv * nb + (int64_t)c.n_points * nv + c.n_points) * sizeof(double) +
-        (size_t)(nb + (int64_t)n_chunks * nb) * sizeof(int32_t);
-    char* ws = nullptr;
-    hipError_t e = hipMallocAsync((void**)&ws, bytes, s);
-    if (e != hipSuccess)
-        return e;
+    const size_t bytes = delta_workspace_bytes(c.N, c.K, c.b_r, c.b_c, c.n_samples, c.n_points);
+    // the caller's workspace, else one allocated (and freed) on the stream
+    char* ws = (char*)c.ws;
+    const bool own = ws == nullptr;
+    hipError_t e = hipSuccess;
+    if (own) {
+        e = hipMallocAsync((void**)&ws, bytes, s);
+        if (e != hipSuccess)
+            return e;
+    } else if (c.ws_bytes < bytes) {
+        return hipErrorInvalidValue;
+    }
     double* scores = (double*)ws;
     double* dots = scores + nb;
     double* q = dots + nv * nb;
@@ -262,7 +279,7 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
             e = hipGetLastError();
         }
     }
-    const hipError_t ef = hipFreeAsync(ws, s);
+    const hipError_t ef = own ? hipFreeAsync(ws, s) : hipSuccess;
     return e != hipSuccess ? e : ef;
 }
 

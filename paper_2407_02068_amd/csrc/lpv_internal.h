@@ -48,6 +48,10 @@ struct lpv_bsr {
     int64_t n_walk;
     int2* walk;            // n_walk: the launch slots' walks, {col | bits << 16 | last << 24, tile}
     void* stream_vals;     // n_tiles * TILE * TILE elements, operand order
+    // workspace of lpv_bsr_grad_w (per-chunk float32 partial sums of every
+    // tile), allocated on the first call and kept until destroy
+    mutable void* gradw_ws;
+    mutable size_t gradw_ws_bytes;
 };
 
 namespace lpv {
@@ -112,7 +116,11 @@ struct DeltaCall {
     int32_t n_points;
     int32_t keep[DELTA_MAX_POINTS];  // kept blocks at each point, non-increasing
     double* delta;                   // n_points, device
+    void* ws;                        // caller workspace, or NULL: allocated per call
+    size_t ws_bytes;
 };
+size_t delta_workspace_bytes(int64_t N, int64_t K, int32_t b_r, int32_t b_c, int64_t n_samples,
+                             int32_t n_points);
 hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s);
 
 // backward.hip
@@ -122,7 +130,10 @@ struct GradWCall {
     const void* X;  // M x K, row stride ldx
     int64_t ldx, M;
     void* dW;  // nnzb x b_r x b_c, BSR order
+    float* ws; // at least grad_w_workspace_bytes(h) bytes
 };
+// Bytes of the weight-gradient workspace of a handle (any M).
+size_t grad_w_workspace_bytes(const lpv_bsr* h);
 hipError_t launch_transpose_blocks(const lpv_bsr* h, void* WT, int64_t ldwt, uint8_t* maskT,
                                    hipStream_t s);
 hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s);

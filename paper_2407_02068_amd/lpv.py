@@ -22,8 +22,9 @@ EPI = {None: 0, "none": 0, "gelu": 1}
 EXPORTED = ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
             "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
             "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_bias_grad_noalloc",
-            "lpv_delta_curve", "lpv_add_layernorm", "lpv_attention", "lpv_bsr_destroy",
-            "lpv_status_str", "lpv_last_error")
+            "lpv_delta_curve", "lpv_delta_curve_ws", "lpv_delta_curve_workspace_size",
+            "lpv_add_layernorm", "lpv_attention", "lpv_bsr_destroy", "lpv_status_str",
+            "lpv_last_error")
 
 
 class LpvError(RuntimeError):
@@ -73,10 +74,15 @@ def lib():
     L.lpv_attention.argtypes = [vp, i64, i32, i32, i32, i32, vp, vp]
     L.lpv_delta_curve.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, vp, i64, i64, i64,
                                   ctypes.c_double, vp, i32, vp, vp]
+    L.lpv_delta_curve_ws.argtypes = [vp, i64, i64, i64, i32, i32, i32, vp, i64, vp, i64, i64,
+                                     i64, ctypes.c_double, vp, i32, vp, vp, ctypes.c_size_t, vp]
+    L.lpv_delta_curve_workspace_size.argtypes = [i64, i64, i32, i32, i64, i32,
+                                                 ctypes.POINTER(ctypes.c_size_t)]
     for f in ("lpv_bsr_pack", "lpv_bsr_info_get", "lpv_bsr_export", "lpv_bsr_schedule_export",
               "lpv_bsr_unpack", "lpv_bsr_linear", "lpv_dense_linear", "lpv_mask_topk",
               "lpv_bsr_transpose", "lpv_bsr_grad_w", "lpv_bias_grad", "lpv_bias_grad_noalloc",
-              "lpv_delta_curve"):
+              "lpv_delta_curve", "lpv_delta_curve_ws", "lpv_delta_curve_workspace_size",
+              "lpv_add_layernorm", "lpv_attention"):
         getattr(L, f).restype = i32
     L.lpv_bsr_destroy.argtypes = [vp]
     L.lpv_bsr_destroy.restype = None
@@ -346,10 +352,23 @@ def bias_grad_noalloc(G, out, stream=None):
     return out
 
 
-def delta_curve(W, grad, samples, b_r, b_c, kappa, pcts, out=None, stream=None):
+def delta_curve_workspace_size(N, K, b_r, b_c, n_samples, n_points):
+    """lpv_delta_curve_workspace_size: bytes of the caller workspace
+    ``delta_curve(..., workspace=)`` needs for this shape."""
+    nbytes = ctypes.c_size_t(0)
+    _check(lib().lpv_delta_curve_workspace_size(N, K, b_r, b_c, n_samples, n_points,
+                                                ctypes.byref(nbytes)),
+           "lpv_delta_curve_workspace_size")
+    return nbytes.value
+
+
+def delta_curve(W, grad, samples, b_r, b_c, kappa, pcts, out=None, stream=None, workspace=None):
     """lpv_delta_curve: the layer's delta curve at the sparsity percentages
     ``pcts`` (non-decreasing).  W, grad: N x K; samples: n x N x K per-sample
-    gradients (same dtype).  Returns a float64 device tensor of len(pcts)."""
+    gradients (same dtype).  Returns a float64 device tensor of len(pcts).
+    With ``workspace`` (a contiguous GPU tensor of at least
+    ``delta_curve_workspace_size`` bytes) it calls lpv_delta_curve_ws, which
+    allocates nothing."""
     if grad.dtype != W.dtype or samples.dtype != W.dtype:
         raise TypeError("W, grad and samples must share a dtype")
     if samples.dim() != 3 or tuple(samples.shape[1:]) != tuple(W.shape) or grad.shape != W.shape:
@@ -365,10 +384,18 @@ def delta_curve(W, grad, samples, b_r, b_c, kappa, pcts, out=None, stream=None):
     gp, ldg = _mat(grad, "grad")
     lds = samples.stride(1) if n > 0 else K
     stride = samples.stride(0) if n > 0 else N * K
-    _check(lib().lpv_delta_curve(wp, ldw, N, K, DTYPES[W.dtype], b_r, b_c, gp, ldg,
-                                 ctypes.c_void_p(samples.data_ptr()), lds, stride, n, float(kappa),
-                                 pc, len(pcts), ctypes.c_void_p(out.data_ptr()), _stream(stream)),
-           "lpv_delta_curve")
+    args = (wp, ldw, N, K, DTYPES[W.dtype], b_r, b_c, gp, ldg,
+            ctypes.c_void_p(samples.data_ptr()), lds, stride, n, float(kappa), pc, len(pcts),
+            ctypes.c_void_p(out.data_ptr()))
+    if workspace is None:
+        _check(lib().lpv_delta_curve(*args, _stream(stream)), "lpv_delta_curve")
+    else:
+        if not isinstance(workspace, torch.Tensor) or not workspace.is_cuda \
+                or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        nbytes = workspace.numel() * workspace.element_size()
+        _check(lib().lpv_delta_curve_ws(*args, ctypes.c_void_p(workspace.data_ptr()), nbytes,
+                                        _stream(stream)), "lpv_delta_curve_ws")
     return out
 
 

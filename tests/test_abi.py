@@ -194,6 +194,33 @@ def test_delta_curve_rejects_bad_arguments(L):
     assert L.lpv_last_error().decode() != ""
 
 
+def test_delta_curve_workspace_size_and_checks(L):
+    sz = ctypes.c_size_t(0)
+
+    def ws(N=3072, K=768, b_r=32, b_c=32, n=4, npt=21, out=True):
+        return L.lpv_delta_curve_workspace_size(N, K, b_r, b_c, n, npt,
+                                                ctypes.byref(sz) if out else None)
+    assert ws() == OK
+    # scores, dots of n + 2 vectors, per-point step sums and terms (float64),
+    # the permutation and the rank counts of 128-block chunks (int32)
+    nb = 96 * 24
+    assert sz.value == (nb + 6 * nb + 21 * 6 + 21) * 8 + (nb + 18 * nb) * 4
+    big = ws(N=768, K=3072, n=64, npt=128) == OK and sz.value
+    assert big > (66 * 2304) * 8
+    assert ws(b_r=8) == BLOCK and ws(N=3072 + 16) == SHAPE and ws(N=1 << 17) == SHAPE
+    assert ws(N=16384, K=16384, b_r=16, b_c=16) == SHAPE
+    assert ws(n=-1) == INVALID and ws(npt=0) == INVALID and ws(npt=129) == INVALID
+    assert ws(out=False) == INVALID
+    pc = (ctypes.c_int32 * 3)(0, 50, 100)
+
+    def dw(buf=FAKE + (4 << 32), nbytes=1 << 30, N=3072):
+        return L.lpv_delta_curve_ws(FAKE, 768, N, 768, 2, 32, 32, FAKE + (1 << 32), 768,
+                                    FAKE + (2 << 32), 768, 3072 * 768, 4, ctypes.c_double(0.1),
+                                    pc, 3, FAKE + (3 << 32), buf, nbytes, None)
+    assert dw(buf=0) == INVALID and dw(nbytes=64) == INVALID and dw(buf=FAKE + 8) == INVALID
+    assert dw(N=3072 + 16) == SHAPE
+
+
 def test_encoder_calls_reject_bad_arguments(L):
     # every check runs before any HIP call; empty batches return OK untouched
     ln = lambda x=FAKE, y=0, M=10, D=768, dt=2, g=FAKE + (1 << 32), b=FAKE + (2 << 32), eps=1e-6, \

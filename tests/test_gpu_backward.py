@@ -146,3 +146,23 @@ def test_backward_headline_sampled():
     assert_close(f64(db), oracle.grad_bias(G, "bf16"), "bf16", "db")
     h.close()
     ht.close()
+
+
+def test_grad_w_reuses_the_handle_workspace():
+    # the handle's workspace is allocated by the first call and reused: three
+    # calls in a row (large M, smaller ragged M, large M again) each match the
+    # oracle, and the first and last agree bit for bit
+    w, G = case(1100, 512, 384, 32, 32, "bf16", cfg=98)
+    h = lpv.bsr_pack(dev(w.W, "bf16"), dev(w.mask), 32, 32)
+    Gd, Xd = dev(G, "bf16"), dev(w.X, "bf16")
+    say("grad_w workspace reuse M=1100, 333, 1100")
+    d1 = lpv.grad_w(h, Gd, Xd)
+    d2 = lpv.grad_w(h, Gd[:333].contiguous(), Xd[:333].contiguous())
+    d3 = lpv.grad_w(h, Gd, Xd)
+    torch.cuda.synchronize()
+    assert_close(f64(d1), oracle.grad_w(G, w.X, "bf16", 32, 32, w.mask), "bf16", "dW 1",
+                 tile=(32, 32))
+    assert_close(f64(d2), oracle.grad_w(G[:333], w.X[:333], "bf16", 32, 32, w.mask), "bf16",
+                 "dW 2", tile=(32, 32))
+    assert torch.equal(d1.view(torch.int16), d3.view(torch.int16))
+    h.close()

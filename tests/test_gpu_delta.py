@@ -83,3 +83,28 @@ def test_delta_curve_widest_rows():
     # 64 KB of LDS
     W, grad, S = inputs(106, 16, 65536, 2, "bf16")
     check(W, grad, S, "bf16", 16, 16, 0.01, [0, 50, 100], "K = 65536")
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_delta_curve_caller_workspace(dtype):
+    # lpv_delta_curve_ws with a caller-owned workspace gives the curve of
+    # lpv_delta_curve bit for bit, on two calls in a row (the second smaller,
+    # the workspace holding the first call's contents)
+    pcts = list(range(0, 101, 5))
+    W, grad, S = inputs(108, 256, 256, 7, dtype)
+    W2, grad2, S2 = inputs(109, 128, 192, 3, dtype)
+    nbytes = lpv.delta_curve_workspace_size(256, 256, 32, 32, 7, len(pcts))
+    assert nbytes >= lpv.delta_curve_workspace_size(128, 192, 16, 32, 3, len(pcts))
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    for (w_, g_, s_, b_r, b_c) in ((W, grad, S, 32, 32), (W2, grad2, S2, 16, 32)):
+        say("delta_curve workspace", dtype, w_.shape, (b_r, b_c), "n=%d" % s_.shape[0])
+        Wd, Gd = dev(w_, dtype), dev(g_, dtype)
+        Sd = dev(s_.reshape(s_.shape[0], -1), dtype).reshape(s_.shape)
+        a = lpv.delta_curve(Wd, Gd, Sd, b_r, b_c, 0.1, pcts)
+        b = lpv.delta_curve(Wd, Gd, Sd, b_r, b_c, 0.1, pcts, workspace=ws)
+        torch.cuda.synchronize()
+        assert torch.equal(a, b)
+        ref = oracle.delta_curve(w_, dtype, b_r, b_c, g_, s_, 0.1, pcts)
+        assert np.abs(b.cpu().numpy() - ref).max() <= TOL * max(np.abs(ref).max(), 1e-300)
+    with pytest.raises(lpv.LpvError):
+        lpv.delta_curve(Wd, Gd, Sd, 16, 32, 0.1, pcts, workspace=ws[:64])
