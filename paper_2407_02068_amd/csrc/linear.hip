@@ -12,7 +12,9 @@
 //
 // One persistent workgroup of 8 waves per compute unit takes items in turn
 // (consecutive items, which share a token tile, go to workgroups on the same
-// XCD so the X slice is fetched from HBM once per XCD L2).  Its steps, across
+// XCD so the X slice is fetched from HBM once per XCD L2); the items of a
+// short last round are cut in two halves of tile rows, each the last item of
+// its own workgroup.  Its steps, across
 // item boundaries, flow through a 4-slot LDS ring:
 //   - gfx950 global->LDS DMA (global_load_lds_dwordx4) stages each step's X
 //     slice [256 tokens x 32 columns] (two instructions per wave) and the
@@ -192,20 +194,59 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // slots and deals them to its C workgroups in turn (c, c + C, ...), so
     // the items of one token tile share that XCD's L2.  Otherwise item
     // x C + c + k P, k = 0, 1, ...: an XCD's workgroups take C consecutive items.
+    //
+    // The last round: after R = n_items / P whole rounds the items left over
+    // (fewer than one per workgroup) would keep a few workgroups busy while
+    // the rest of the chip idles.  When at most half of the workgroups (of the
+    // XCD, in the XCD order) would get one, each is cut into its two halves of
+    // tile rows (4 hh .. 4 hh + 3 of the group, hh = 0, 1), run as the last
+    // item of two workgroups: the same steps, with the other half's row bits
+    // cleared, so half the W and half the matrix-core work per SIMD (each
+    // SIMD runs one wave of either half), and half the stores.
     const int P = (int)gridDim.x, C = P >> 3;
     const int xcd = (int)(blockIdx.x & 7), cu = (int)(blockIdx.x >> 3);
+    const int R = a.n_items / P;
     int first_mt, first_slot, my_items;
+    int h_mt = 0, h_slot = 0, hh = -1;  // the half item (row half hh), if any
     if (a.xcd_tiles) {
         const int n_mt = a.n_items / a.n_slots;
         const int n_local = xcd < n_mt ? (n_mt - xcd + 7) / 8 * a.n_slots : 0;
         my_items = cu < n_local ? (n_local - cu + C - 1) / C : 0;
         first_mt = xcd + 8 * (cu / a.n_slots);
         first_slot = cu % a.n_slots;
+        const int tail = n_local - C * R;
+        if (tail > 0 && 2 * tail <= C) {
+            my_items = R;
+            if (cu < 2 * tail) {
+                const int li = C * R + cu / 2;
+                h_mt = xcd + 8 * (li / a.n_slots);
+                h_slot = li % a.n_slots;
+                hh = cu & 1;
+            }
+        }
     } else {
         const int item_off = xcd * C + cu;
         my_items = item_off < a.n_items ? (a.n_items - item_off + P - 1) / P : 0;
         first_mt = item_off / a.n_slots;
         first_slot = item_off % a.n_slots;
+        const int tail = a.n_items - P * R;
+        if (tail > 0 && 2 * tail <= P) {
+            my_items = R;
+            if (item_off < 2 * tail) {
+                const int i = P * R + item_off / 2;
+                h_mt = i / a.n_slots;
+                h_slot = i % a.n_slots;
+                hh = item_off & 1;
+            }
+        }
+    }
+    const int n_full = my_items;  // whole items; the half item, if any, comes last
+    if (hh >= 0) {
+        if (n_full == 0) {
+            first_mt = h_mt;
+            first_slot = h_slot;
+        }
+        ++my_items;
     }
     if (my_items == 0)
         return;
@@ -347,7 +388,10 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         if (pk >= my_items)
             return 0;
         const int ex = __builtin_amdgcn_readlane(cur.x, p_i);
-        const int col = ex & 0xffff, bits = (ex >> 16) & 0xff;
+        const int col = ex & 0xffff, all_bits = (ex >> 16) & 0xff;
+        // a half item keeps its own half's rows (the tile stream order, and so
+        // a tile's rank, still counts every kept row of the step)
+        const int bits = pk == n_full ? all_bits & (0xf << (4 * hh)) : all_bits;
         d.col = col;
         d.xcol = (uint32_t)col * (TILE * 2);
         d.n = bits ? 2 : 0;  // a step that keeps no tile (walk padding) loads nothing
@@ -356,7 +400,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
                 d.n = 4;
         } else if ((bits >> wave) & 1) {  // row `wave` of the group is kept: its tile
             // (the stream holds fewer than 2^21 tiles: the offset fits 32 bits)
-            const int rank = __popc(bits & ((1 << wave) - 1));
+            const int rank = __popc(all_bits & ((1 << wave) - 1));
             d.woff = (uint32_t)(__builtin_amdgcn_readlane(cur.y, p_i) + rank) * 2048u;
             d.n = 4;
         }
@@ -371,11 +415,20 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             ++p_i;
         }
         if ((ex & W_LAST) && ++pk < my_items) {
-            p_slot += a.p_mod;
-            p_mt += a.p_div;
-            if (p_slot >= a.n_slots) {
-                p_slot -= a.n_slots;
-                p_mt += a.mt_carry;
+            if (pk == n_full) {
+                // on to the half item: its walk replaces the prefetched one
+                p_slot = h_slot;
+                p_mt = h_mt;
+                cur = seg_read(t_desc[h_slot].y);
+                nxt = seg_read(__builtin_amdgcn_readlane(cur.z, 0));
+                p_i = 0;
+            } else {
+                p_slot += a.p_mod;
+                p_mt += a.p_div;
+                if (p_slot >= a.n_slots) {
+                    p_slot -= a.n_slots;
+                    p_mt += a.mt_carry;
+                }
             }
             x_stale = true;
         }
@@ -586,7 +639,9 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     v4i pko[2][4][2];  // (token half u, tile row j, p2): outputs 32 j + 16 p2 + 8 h + 0..7
     int64_t f_mw = 0, f_nw = 0;  // the packed item's first token and output of this wave
     bool f_inside = true;        // ... and whether its whole tile lies inside Y
+    bool f_skip = false;         // ... and whether it is a half item of the other half
     auto pack = [&]() {
+        f_skip = ck == n_full && wh != hh;
         const v4i cd = lds_read16<0>(desc_lds + c_slot * 16);
         const int c_g = __builtin_amdgcn_readfirstlane(cd.x);
         f_mw = (int64_t)c_mt * BM + wm * 64;
@@ -624,6 +679,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         }
     };
     auto flush = [&](int sslot) {
+        if (f_skip)
+            return;
         const int64_t mw = f_mw, nw = f_nw;
         const bool inside = f_inside;
         // staging: token tau (0..31) of a round at region tau / 16 of this
@@ -721,11 +778,16 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         have = true;
         if (++ck >= my_items)
             break;
-        c_slot += a.p_mod;
-        c_mt += a.p_div;
-        if (c_slot >= a.n_slots) {
-            c_slot -= a.n_slots;
-            c_mt += a.mt_carry;
+        if (ck == n_full) {
+            c_slot = h_slot;
+            c_mt = h_mt;
+        } else {
+            c_slot += a.p_mod;
+            c_mt += a.p_div;
+            if (c_slot >= a.n_slots) {
+                c_slot -= a.n_slots;
+                c_mt += a.mt_carry;
+            }
         }
     }
     flush(((t - 1) >> 1) & 1);

@@ -307,6 +307,29 @@ def test_multi_launch_tables(N, K):
     assert_close(f64(Yd), r, "bf16", "dense " + w.name)
 
 
+@pytest.mark.parametrize("dense", [False, True])
+def test_last_round_split(dense):
+    """38 token tiles x 12 output groups: with 256 compute units, 8 XCDs of 32
+    workgroups, XCDs 0-5 own 5 token tiles (60 items: one whole round of 32
+    and 28 left, too many to halve) and XCDs 6-7 own 4 (48 items: 16 left,
+    each run as two half items).  Rows of tiles on both kinds of XCD are
+    checked against the oracle, for the block-sparse and the dense launch."""
+    w = wl.custom(78, 38 * 256, 3072, 768, 32, 32, "bf16", "uniform", 0 if dense else 50)
+    say("last round split", "dense" if dense else "sparse", "M", w.M, "nnzb", w.nnzb)
+    if dense:
+        Y = lpv.dense_linear(dev(w.W, "bf16"), dev(w.X, "bf16"), dev(w.bias, "bf16"))
+        torch.cuda.synchronize()
+    else:
+        _, Y = run_bsr(w)
+    g = np.random.default_rng(79)
+    rows = []
+    for tile in (0, 6, 7, 14, 30, 31, 37):
+        rows += [tile * 256, tile * 256 + 255] + (tile * 256 + g.choice(256, 14, replace=False)).tolist()
+    rows = np.array(sorted(set(rows)))
+    r = ref(w, X=w.X[rows])
+    assert_close(f64(Y[torch.from_numpy(rows).cuda()]), r, "bf16", w.name + " sampled")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f16"])
 def test_zipf_many_token_tiles(dtype):
     """Skewed (Zipf) row keep counts with more than 8 token tiles of 256, so the
