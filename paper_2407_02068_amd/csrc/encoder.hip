@@ -91,83 +91,156 @@ __global__ __launch_bounds__(256) void k_add_layernorm(const uint16_t* x, const 
 
 // ---------------------------------------------------------------- attention
 
-// One workgroup per (sequence, head), 4 waves; wave w takes the 32-query tiles
-// w, w + 4, ...  With Q and K both token-major, S^T = K Q^T comes from the
-// matrix cores straight from global memory (lane: key or query l % 32, 8
-// consecutive head dimensions).  Its accumulator gives lane l query l % 32 and,
-// in register r, key 8 (r / 4) + 4 (l / 32) + r % 4 of the 32-key tile: a row
-// of softmax lives in two lanes (l and l ^ 32), so the online softmax (running
-// maximum m, running sum l, rescale by 2^(m_old - m_new)) needs one lane swap.
-// The weights P^T, rounded once, are already the B operand of O^T = V^T P^T
-// when the k slots of the two 16-key steps are read as those keys; V^T (A
-// operand: lane = head dimension, 8 keys in two runs of 4) is staged once per
-// workgroup in LDS, transposed, zero past the last token.  O^T's accumulator
-// again holds one query per lane, so the rescale and the final 1 / l are
-// per lane.  The weights summed into l are the rounded ones, so the output is
-// exactly a weighted mean of V with those weights.
+// One workgroup per (sequence, head), 8 waves.  K and V of the head are staged
+// once in LDS, row-major (row = token, 64 elements and 16 bytes of padding:
+// 144-byte rows put 16 consecutive rows of one 16-byte column in distinct
+// banks), zero past the last token; wave w takes the 32-query tiles w, w + 8,
+// ...  S^T = K Q^T on the matrix cores (lane: key or query l % 32, 8
+// consecutive head dimensions; K from LDS, Q from global memory once per
+// tile).  Its accumulator gives lane l query l % 32 and, in register r, key
+// 8 (r / 4) + 4 (l / 32) + r % 4 of the 32-key tile: a row of softmax lives
+// in two lanes (l and l ^ 32), so the online softmax (running maximum m,
+// running sum l, rescale by 2^(m_old - m_new)) needs one lane swap.  The
+// weights P^T, rounded once, are already the B operand of O^T = V^T P^T when
+// the k slots of the two 16-key steps are read as those keys; the V^T operand
+// (lane = head dimension, 8 keys in two runs of 4) comes from the row-major V
+// by transposing LDS reads (ds_read_b64_tr_b16: within 16 lanes, lane j
+// reads key t0 + j / 4 at dimensions c0 + 4 (j % 4) .. + 3, and lane i
+// receives keys t0 .. t0 + 3 of dimension c0 + i).  O^T's accumulator again
+// holds one query per lane, so the rescale and the final 1 / l are per lane.
+// The weights summed into l are the rounded ones, so the output is exactly a
+// weighted mean of V with those weights.
+constexpr int ATT_NT = 512;
+constexpr int ATT_RS = ATT_HD * 2 + 16;  // bytes per staged row
+static_assert(2 * ((ATT_MAX_T + 31) / 32 * 32) * ATT_RS <= 163840, "K and V of a head fit in LDS");
+
+typedef short att_v4s __attribute__((ext_vector_type(4)));
+
+__device__ inline uint2 att_tr_read(uint32_t addr)
+{
+    return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                                         (__attribute__((address_space(3))) att_v4s*)(uintptr_t)addr));
+}
+
+typedef unsigned int att_u4 __attribute__((ext_vector_type(4)));
+
+// c + the two 16-bit values packed in p (one dot product with (1, 1): the
+// products are exact, the sum is float32)
+template <int DT> __device__ inline float att_add2(uint32_t p, float c)
+{
+    if (DT == LPV_BF16)
+        return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, p),
+                                               __builtin_bit_cast(bf16x2, 0x3f803f80u), c, false);
+    return __builtin_amdgcn_fdot2(__builtin_bit_cast(f16x2, p), __builtin_bit_cast(f16x2, 0x3c003c00u),
+                                  c, false);
+}
+
+__device__ inline uint4 att_read16(uint32_t addr)
+{
+    return __builtin_bit_cast(uint4, *(const __attribute__((address_space(3))) att_u4*)(uintptr_t)addr);
+}
+
 template <int DT>
-__global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ qkv, int32_t T,
-                                                   int32_t H, uint16_t* __restrict__ out)
+__global__ __launch_bounds__(ATT_NT) void k_attention(const uint16_t* __restrict__ qkv, int32_t T,
+                                                      int32_t H, uint16_t* __restrict__ out)
 {
     using E = Elem<DT>;
     using F = typename E::frag;
-    extern __shared__ uint16_t vt[];  // [64][Tp]
+    extern __shared__ uint4 att_lds[];  // K rows, then V rows
     const int seq = blockIdx.x / H, h = blockIdx.x - seq * H;
-    const int n_kt = (T + 31) / 32, Tp = 32 * n_kt + 4;  // + 4: rows start 8 bytes apart in banks
+    const int n_kt = (T + 31) / 32, Tp = 32 * n_kt;
     const int64_t ld = 3 * (int64_t)H * ATT_HD, ldo = (int64_t)H * ATT_HD;
     const uint16_t* base = qkv + (int64_t)seq * T * ld;
-
-    for (int i = threadIdx.x; i < n_kt * 32 * 8; i += 256) {
-        const int s = i >> 3, c = i & 7;
-        uint4 v = {0u, 0u, 0u, 0u};
-        if (s < T)
-            v = *(const uint4*)(base + s * ld + 2 * ldo + h * ATT_HD + 8 * c);
-        const uint16_t* e = (const uint16_t*)&v;
-#pragma unroll
-        for (int j = 0; j < 8; ++j)
-            vt[(8 * c + j) * Tp + s] = e[j];
-    }
-    __syncthreads();
+    char* kl = (char*)att_lds;
+    char* vl = kl + Tp * ATT_RS;
 
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int l32 = lane & 31, half = lane >> 5;
-    const float scale = 0.125f * 1.44269504088896340736f;  // 1 / sqrt(64), in base 2
-    for (int qt = wave; qt < n_kt; qt += 4) {
-        const int q = qt * 32 + l32;
-        const uint16_t* qrow = base + (int64_t)min(q, T - 1) * ld + h * ATT_HD + 8 * half;
-        F qf[4];
+    // the Q fragments of this wave's first query tile, loaded while K and V
+    // are staged (lane: query l % 32, dimensions 8 half + 16 ks)
+    F qf[4];
+    auto load_q = [&](int qt) {
+        const uint16_t* qrow =
+            base + (int64_t)min(qt * 32 + l32, T - 1) * ld + h * ATT_HD + 8 * half;
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks)
             qf[ks] = as_frag<F>(*(const uint4*)(qrow + 16 * ks));
-        f32x16 o[2] = {f32x16{}, f32x16{}};
-        float m = -INFINITY, l = 0.0f;
-        for (int kt = 0; kt < n_kt; ++kt) {
-            const uint16_t* krow =
-                base + (int64_t)min(kt * 32 + l32, T - 1) * ld + ldo + h * ATT_HD + 8 * half;
-            F kf[4];
+    };
+    if (wave < n_kt)
+        load_q(wave);
+    // staging: 16-byte chunk c (0..7) of row s of K and V; every load of a
+    // batch is issued before the first LDS write
+    constexpr int SB = 4;
+    for (int i0 = threadIdx.x; i0 < Tp * 8; i0 += SB * ATT_NT) {
+        uint4 kv[SB], vv[SB];
 #pragma unroll
-            for (int ks = 0; ks < 4; ++ks)
-                kf[ks] = as_frag<F>(*(const uint4*)(krow + 16 * ks));
+        for (int b = 0; b < SB; ++b) {
+            const int i = i0 + b * ATT_NT, s = i >> 3, c = i & 7;
+            kv[b] = uint4{0u, 0u, 0u, 0u};
+            vv[b] = uint4{0u, 0u, 0u, 0u};
+            if (s < T) {
+                const uint16_t* row = base + (int64_t)s * ld + h * ATT_HD + 8 * c;
+                kv[b] = *(const uint4*)(row + ldo);
+                vv[b] = *(const uint4*)(row + 2 * ldo);
+            }
+        }
+#pragma unroll
+        for (int b = 0; b < SB; ++b) {
+            const int i = i0 + b * ATT_NT, s = i >> 3, c = i & 7;
+            if (i < Tp * 8) {
+                *(uint4*)(kl + s * ATT_RS + 16 * c) = kv[b];
+                *(uint4*)(vl + s * ATT_RS + 16 * c) = vv[b];
+            }
+        }
+    }
+    __syncthreads();
+
+    // this lane's K fragment (key l32 of a tile, dimensions 8 half + 16 ks)
+    const uint32_t ka = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)kl +
+                        l32 * ATT_RS + half * 16;
+    // this lane's transposing V read: 16-lane group g = lane / 16 takes
+    // dimensions 16 (g % 2) + 0..15 (of 32 dt + ..) and keys 4 (g / 2) + 0..3
+    // (of the 16-key step; + 8 for the second run)
+    const int g = lane >> 4, jj = lane & 15;
+    const uint32_t va = (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) char*)vl +
+                        ((jj >> 2) + 4 * (g >> 1)) * ATT_RS + (16 * (g & 1) + 4 * (jj & 3)) * 2;
+    const float scale = 0.125f * 1.44269504088896340736f;  // 1 / sqrt(64), in base 2
+    for (int qt = wave; qt < n_kt; qt += ATT_NT / 64) {
+        const int q = qt * 32 + l32;
+        if (qt != wave)
+            load_q(qt);
+        f32x16 o[2] = {f32x16{}, f32x16{}};
+        float m = -INFINITY, l = 0.0f;  // running maximum of the unscaled scores, sum
+        for (int kt = 0; kt < n_kt; ++kt) {
+            const uint32_t kt_off = (uint32_t)kt * 32 * ATT_RS;
             f32x16 s = {};
 #pragma unroll
             for (int ks = 0; ks < 4; ++ks)
-                s = E::mma(kf[ks], qf[ks], s);
-            float mt = -INFINITY;
+                s = E::mma(as_frag<F>(att_read16(ka + kt_off + 32 * ks)), qf[ks], s);
+            if (kt == n_kt - 1 && T % 32) {  // the last tile: keys past T drop out
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                const int key = kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3);
-                s[r] = key < T ? s[r] * scale : -INFINITY;
-                mt = fmaxf(mt, s[r]);
+                for (int r = 0; r < 16; ++r)
+                    if (kt * 32 + 8 * (r >> 2) + 4 * half + (r & 3) >= T)
+                        s[r] = -INFINITY;
             }
+            float mt = s[0];
+#pragma unroll
+            for (int r = 1; r < 16; ++r)
+                mt = fmaxf(mt, s[r]);
             mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
             const float mn = fmaxf(m, mt);  // finite: every tile has a key
-            const float alpha = exp2f(m - mn);
+            // weights 2^((s - mn) scale): the scale is positive, so the maximum
+            // of the scaled scores is the scaled maximum (arguments <= 0; the
+            // hardware exp2 flushes results below 2^-126 to zero)
+            const float nms = -mn * scale;
+            const float alpha = __builtin_amdgcn_exp2f((m - mn) * scale);
             uint32_t pb[8];
             float ps = 0.0f;
 #pragma unroll
             for (int j = 0; j < 8; ++j) {
-                pb[j] = pack2<DT>(exp2f(s[2 * j] - mn), exp2f(s[2 * j + 1] - mn));
-                ps += E::to_f32((uint16_t)(pb[j] & 0xffffu)) + E::to_f32((uint16_t)(pb[j] >> 16));
+                pb[j] = pack2<DT>(__builtin_amdgcn_exp2f(fmaf(s[2 * j], scale, nms)),
+                                  __builtin_amdgcn_exp2f(fmaf(s[2 * j + 1], scale, nms)));
+                ps = att_add2<DT>(pb[j], ps);
             }
             ps += __shfl_xor(ps, 32, 64);
             l = l * alpha + ps;
@@ -179,8 +252,8 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
                 const F pf = as_frag<F>(uint4{pb[4 * st], pb[4 * st + 1], pb[4 * st + 2], pb[4 * st + 3]});
 #pragma unroll
                 for (int dt = 0; dt < 2; ++dt) {
-                    const uint16_t* vp = vt + (32 * dt + l32) * Tp + kt * 32 + 16 * st + 4 * half;
-                    const uint2 lo = *(const uint2*)vp, hi = *(const uint2*)(vp + 8);
+                    const uint32_t vp = va + kt_off + (uint32_t)(16 * st) * ATT_RS + 64 * dt;
+                    const uint2 lo = att_tr_read(vp), hi = att_tr_read(vp + 8 * ATT_RS);
                     o[dt] = E::mma(as_frag<F>(uint4{lo.x, lo.y, hi.x, hi.y}), pf, o[dt]);
                 }
             }
@@ -191,10 +264,10 @@ __global__ __launch_bounds__(256) void k_attention(const uint16_t* __restrict__ 
 #pragma unroll
             for (int dt = 0; dt < 2; ++dt)
 #pragma unroll
-                for (int g = 0; g < 4; ++g)
-                    *(uint2*)(orow + 32 * dt + 8 * g + 4 * half) =
-                        uint2{pack2<DT>(o[dt][4 * g] * inv, o[dt][4 * g + 1] * inv),
-                              pack2<DT>(o[dt][4 * g + 2] * inv, o[dt][4 * g + 3] * inv)};
+                for (int gg = 0; gg < 4; ++gg)
+                    *(uint2*)(orow + 32 * dt + 8 * gg + 4 * half) =
+                        uint2{pack2<DT>(o[dt][4 * gg] * inv, o[dt][4 * gg + 1] * inv),
+                              pack2<DT>(o[dt][4 * gg + 2] * inv, o[dt][4 * gg + 3] * inv)};
         }
     }
 }
@@ -225,14 +298,14 @@ hipError_t launch_attention(const void* qkv, int64_t n_seq, int32_t T, int32_t H
     if (n_seq == 0)
         return hipSuccess;
     const int n_kt = (T + 31) / 32;
-    const size_t lds = (size_t)ATT_HD * (32 * n_kt + 4) * 2;
-    const dim3 grid((unsigned)(n_seq * H)), block(256);
-    // dynamic LDS beyond 64 KB (T > 480) must be allowed per kernel; the
+    const size_t lds = (size_t)2 * 32 * n_kt * ATT_RS;
+    const dim3 grid((unsigned)(n_seq * H)), block(ATT_NT);
+    // dynamic LDS beyond 64 KB (T > 224) must be allowed per kernel; the
     // setting is idempotent, so a race between threads is harmless
     static bool allowed[2] = {false, false};
     const int ix = dtype == LPV_BF16 ? 1 : 0;
     if (!allowed[ix]) {
-        const int max_lds = ATT_HD * (ATT_MAX_T + 4) * 2;
+        const int max_lds = 2 * ((ATT_MAX_T + 31) / 32 * 32) * ATT_RS;
         const hipError_t e =
             dtype == LPV_BF16
                 ? hipFuncSetAttribute((const void*)k_attention<LPV_BF16>,

@@ -140,7 +140,7 @@ hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s);
 // Encoder block around the pruned layers (encoder.hip).
 constexpr int LN_MAX_D = 2048;     // widest row of the layer norm
 constexpr int ATT_HD = 64;         // head dimension of the attention kernel
-constexpr int ATT_MAX_T = 512;     // longest sequence (V^T staged in LDS)
+constexpr int ATT_MAX_T = 512;     // longest sequence (K and V staged in LDS)
 hipError_t launch_add_layernorm(const void* x, const void* y, int64_t M, int32_t D, int dtype,
                                 const void* gamma, const void* beta, float eps, void* S, void* out,
                                 hipStream_t s);
