@@ -14,30 +14,30 @@
 // (consecutive items, which share a token tile, go to workgroups on the same
 // XCD so the X slice is fetched from HBM once per XCD L2); the items of a
 // short last round are cut in two halves of tile rows, each the last item of
-// its own workgroup.  Its steps, across
-// item boundaries, flow through a 4-slot LDS ring:
-//   - gfx950 global->LDS DMA (global_load_lds_dwordx4) stages each step's X
-//     slice [256 tokens x 32 columns] (two instructions per wave) and the
-//     step's kept W tiles (tile j by wave j, two instructions), 3 steps ahead,
-//     16 bytes per lane with no registers in between;
-//   - a wave's DMA count per step is 2 or 4, known from the step's row bits,
-//     which travel from the producer cursor to the consumer in a 64-bit queue
-//     (16 bits per step in flight); the wait before each step's barrier
-//     leaves exactly the later steps' DMA (and a finished item's stores) in
-//     flight, and the barrier tells every wave that the whole step landed;
+// its own workgroup.  Its steps, across item boundaries, go in pairs through
+// two LDS pair slots, one barrier per pair:
+//   - gfx950 global->LDS DMA (global_load_lds_dwordx4) stages a pair's X
+//     slices [256 tokens x 2 x 32 columns] (four instructions per wave) and
+//     the pair's kept W tiles (tile j by wave j, two instructions per step),
+//     one pair ahead, 16 bytes per lane with no registers in between;
+//   - each step's row bits travel from the producer cursor to the consumer in
+//     a 64-bit queue (12 bits per step in flight); the wait before each pair's
+//     barrier (vmcnt(0)) covers the next pair's DMA and a finished item's
+//     stores, and the barrier tells every wave that the pair landed and that
+//     the pair slot read before it is free;
 //   - wave (m, h) takes tokens [64m, 64m + 64) and tile rows [4h, 4h + 4) of
 //     the group and issues v_mfma_f32_32x32x16 (bf16 / fp16 in, float32
 //     accumulate) for each kept tile; the two waves of a SIMD cover both row
-//     halves, so every SIMD gets the step's whole kept count.  The h = 1 wave
-//     reads its operands before the barrier and the h = 0 wave after it, so
-//     one wave's LDS reads overlap the other's matrix-core work.
+//     halves, so every SIMD gets the step's whole kept count.  Each half step
+//     reads the next half step's fragments while its own go to the matrix
+//     cores.
 // The step loop carries no division and no scalar load on its critical path:
 // the per-group descriptors (group, first step, step count, first column
 // walked) are built at pack time, item coordinates advance by constants, and
-// the next step's metadata is loaded one step ahead.
+// the walk is read one 64-entry segment ahead.
 // The epilogue adds the bias, applies GELU if asked, rounds once to the element
 // type and stores Y (16 bytes per lane, transposed through LDS), while the DMA
-// of the next item's first steps is already in flight.
+// of the next item's first pair is already in flight.
 //
 // MFMA operand roles: A = a W tile (rows = output features), B = X slice
 // transposed (columns = tokens), so D[n][token]: lane l holds token l % 32 and,
