@@ -59,6 +59,7 @@ __global__ __launch_bounds__(256) void k_rank_scatter(const int32_t* __restrict_
     if (b >= nb)
         return;
     int64_t rank = 0;
+#pragma unroll 8
     for (int j = 0; j < n_chunks; ++j)
         rank += cnt[(int64_t)j * nb + b];
     perm[rank] = (int32_t)b;
@@ -85,57 +86,76 @@ template <int DT> __device__ inline void load8(const char* base, int64_t idx, do
 
 // dots[v][r C + c] = sum over block (r, c) of x_v[e] * (-W[e]), float64:
 // x_v = sample v (v < n_samples), grad (v = n_samples), W (v = n_samples + 1).
-// Workgroup (block-row r, vector v).  The block-row's 8-element column chunks
+// Workgroup (block-row r, vectors VPW y .. VPW y + VPW - 1): each W chunk is
+// loaded once for its VPW vectors.  The block-row's 8-element column chunks
 // (nch = K / 8) are spread over the threads; when nch < 256 the rows are split
 // into G = 256 / nch interleaved groups as well.  Thread (g, q) sums chunk q
 // over rows g, g + G, ... (ascending); a block's sum then adds its chunks' sums
 // group by group, in column order.
-template <int DT>
+template <int DT, int VPW>
 __global__ __launch_bounds__(256) void k_delta_dots(const DeltaCall c, int32_t C,
                                                     double* __restrict__ dots)
 {
-    extern __shared__ double s_part[];  // G x nch chunk sums
+    extern __shared__ double s_part[];  // VPW x G x nch chunk sums
     constexpr int ES = DT == LPV_F32 ? 4 : 2;
     const int r = blockIdx.x;
-    const int64_t v = blockIdx.y;
-    const char* x;
-    int64_t ldx;
-    if (v < c.n_samples) {
-        x = (const char*)c.samples + v * c.stride * ES;
-        ldx = c.lds;
-    } else if (v == c.n_samples) {
-        x = (const char*)c.grad;
-        ldx = c.ldg;
-    } else {
-        x = (const char*)c.W;
-        ldx = c.ldw;
+    const int64_t nv = c.n_samples + 2, v0 = (int64_t)blockIdx.y * VPW;
+    const int nvv = (int)min((int64_t)VPW, nv - v0);
+    const char* xs[VPW];
+    int64_t lx[VPW];
+#pragma unroll
+    for (int u = 0; u < VPW; ++u) {
+        const int64_t v = min(v0 + u, nv - 1);
+        if (v < c.n_samples) {
+            xs[u] = (const char*)c.samples + v * c.stride * ES;
+            lx[u] = c.lds;
+        } else if (v == c.n_samples) {
+            xs[u] = (const char*)c.grad;
+            lx[u] = c.ldg;
+        } else {
+            xs[u] = (const char*)c.W;
+            lx[u] = c.ldw;
+        }
     }
     const char* w = (const char*)c.W;
     const int nch = (int)(c.K / 8);
     const int G = nch >= 256 ? 1 : 256 / nch;
     for (int t = threadIdx.x; t < G * nch; t += 256) {
         const int g = t / nch, q = t - g * nch;
-        double acc = 0.0;
-#pragma unroll 4
+        double acc[VPW];
+#pragma unroll
+        for (int u = 0; u < VPW; ++u)
+            acc[u] = 0.0;
+#pragma unroll 2
         for (int i = g; i < c.b_r; i += G) {
             const int64_t row = (int64_t)r * c.b_r + i;
-            double xv[8], wv[8];
-            load8<DT>(x, row * ldx + (int64_t)q * 8, xv);
+            double wv[8];
             load8<DT>(w, row * c.ldw + (int64_t)q * 8, wv);
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                acc += xv[j] * -wv[j];
+            for (int u = 0; u < VPW; ++u) {
+                if (u < nvv) {
+                    double xv[8];
+                    load8<DT>(xs[u], row * lx[u] + (int64_t)q * 8, xv);
+#pragma unroll
+                    for (int j = 0; j < 8; ++j)
+                        acc[u] += xv[j] * -wv[j];
+                }
+            }
         }
-        s_part[t] = acc;
+#pragma unroll
+        for (int u = 0; u < VPW; ++u)
+            s_part[u * G * nch + t] = acc[u];
     }
     __syncthreads();
     const int per = c.b_c / 8;
-    for (int cc = threadIdx.x; cc < C; cc += 256) {
+    for (int i = threadIdx.x; i < nvv * C; i += 256) {
+        const int u = i / C, cc = i - u * C;
+        const double* sp = s_part + u * G * nch;
         double s = 0.0;
         for (int g = 0; g < G; ++g)
             for (int q = 0; q < per; ++q)
-                s += s_part[g * nch + cc * per + q];
-        dots[v * ((int64_t)(c.N / c.b_r) * C) + (int64_t)r * C + cc] = s;
+                s += sp[g * nch + cc * per + q];
+        dots[(v0 + u) * ((int64_t)(c.N / c.b_r) * C) + (int64_t)r * C + cc] = s;
     }
 }
 
@@ -175,8 +195,11 @@ __global__ __launch_bounds__(1024) void k_delta_finish(const DeltaCall c, double
                                                        double* __restrict__ term)
 {
     const int64_t nv = c.n_samples + 2;
+    // (the loads of each loop are independent of its running sums: unrolled,
+    // they are issued ahead of the additions)
     for (int64_t v = threadIdx.x; v < c.n_samples; v += 1024) {
         double a = 0.0;
+#pragma unroll 8
         for (int k = 0; k < c.n_points; ++k) {
             const double b = bsum[(int64_t)k * nv + v];
             bsum[(int64_t)k * nv + v] = (0.5 * b + a) * b;
@@ -187,6 +210,7 @@ __global__ __launch_bounds__(1024) void k_delta_finish(const DeltaCall c, double
     for (int k = threadIdx.x; k < c.n_points; k += 1024) {
         const double* qk = bsum + (int64_t)k * nv;
         double f = 0.0;
+#pragma unroll 16
         for (int64_t v = 0; v < c.n_samples; ++v)
             f += qk[v];
         // grad . d, and |d|^2 = -(W . (-W)) over the step
@@ -258,15 +282,26 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
         }
     }
     if (e == hipSuccess) {
-        const dim3 grid((unsigned)R, (unsigned)nv);
         const int64_t nch = c.K / 8;
-        const size_t lds = (size_t)(nch >= 256 ? nch : 256 / nch * nch) * sizeof(double);
+        const int64_t part = (nch >= 256 ? nch : 256 / nch * nch) * (int64_t)sizeof(double);
+        // vectors per workgroup: 4 while their chunk sums fit 64 KB of LDS
+        const int vpw = part * 4 <= 65536 ? 4 : 1;
+        const dim3 grid((unsigned)R, (unsigned)((nv + vpw - 1) / vpw));
+        const size_t lds = (size_t)(part * vpw);
+#define LPV_DOTS(DT_)                                                                         \
+    do {                                                                                      \
+        if (vpw == 4)                                                                         \
+            hipLaunchKernelGGL((k_delta_dots<DT_, 4>), grid, dim3(256), lds, s, c, C, dots); \
+        else                                                                                  \
+            hipLaunchKernelGGL((k_delta_dots<DT_, 1>), grid, dim3(256), lds, s, c, C, dots); \
+    } while (0)
         if (c.dtype == LPV_BF16)
-            hipLaunchKernelGGL(k_delta_dots<LPV_BF16>, grid, dim3(256), lds, s, c, C, dots);
+            LPV_DOTS(LPV_BF16);
         else if (c.dtype == LPV_F16)
-            hipLaunchKernelGGL(k_delta_dots<LPV_F16>, grid, dim3(256), lds, s, c, C, dots);
+            LPV_DOTS(LPV_F16);
         else
-            hipLaunchKernelGGL(k_delta_dots<LPV_F32>, grid, dim3(256), lds, s, c, C, dots);
+            LPV_DOTS(LPV_F32);
+#undef LPV_DOTS
         e = hipGetLastError();
     }
     if (e == hipSuccess) {
