@@ -121,7 +121,9 @@ def kernel_label(name):
             "dense" if m.group(3) == "true" else "block-sparse",
             " + GELU" if m.group(2) == "true" else "", ", K tail" if m.group(4) == "true" else "",
             "lpv_dense_linear" if m.group(3) == "true" else "lpv_bsr_linear")
-    labels = (("k_block_scores<2, true", "k_block_scores, Taylor (lpv_delta_curve)"),
+    labels = (("k_block_scores_lds<2, true", "k_block_scores_lds, Taylor (lpv_delta_curve)"),
+              ("k_block_scores_lds<2, false", "k_block_scores_lds, sum of squares (lpv_mask_topk)"),
+              ("k_block_scores<2, true", "k_block_scores, Taylor (lpv_delta_curve)"),
               ("k_block_scores<2, false", "k_block_scores, sum of squares (lpv_mask_topk)"),
               ("k_block_scores", "k_block_scores (lpv_mask_topk)"),
               ("k_delta_dots", "k_delta_dots (lpv_delta_curve)"),
@@ -215,12 +217,15 @@ def write_stats(stats_csv, command, backward=False, trace_csv=None, bench_log=No
         text += ["", "The block-sparse k_linear16 row counts the forward launches and the dX "
                  "launches (the same kernel on the transposed handle).  dW is k_gradw_tiles + "
                  "k_gradw_reduce, db k_bias_partial + k_bias_reduce, the delta curve "
-                 "k_block_scores + k_rank_counts + k_rank_scatter + k_delta_dots + "
+                 "k_block_scores_lds + k_rank_counts + k_rank_scatter + k_delta_dots + "
                  "k_delta_steps + k_delta_finish; Cijk_Ailk is hipBLASLt's dense G^T X "
                  "reference, Custom_Cijk_Alik its dense forward."]
     else:
         text += ["", "Rows of one kernel name cover every shape the run launches it at (the "
-                 "headline, the sweep, the encoder's linears).  The hipBLASLt rows (Cijk) are "
+                 "headline, the sweep, the encoder's linears).  The encoder leg (12-block DeiT-B, "
+                 "batch 256: chains with block-sparse and with dense linears, attention and layer "
+                 "norm timed alone, the power windows) accounts for the k_attention and "
+                 "k_add_layernorm rows.  The hipBLASLt rows (Cijk) are "
                  "`torch.addmm` at the headline shape, a check on the dense path."]
     with open(STATS_FILE_BACKWARD if backward else STATS_FILE, "w") as f:
         f.write("\n".join(text) + "\n")
