@@ -102,8 +102,10 @@ typedef struct {
  *
  * Allocates device memory (freed by lpv_bsr_destroy) and waits once on
  * `stream` to learn the kept count.  W and mask may be freed afterwards.
- * bf16 / fp16: at most 2^21 - 1 kept 32 x 32 tiles (SHAPE otherwise; the
- * kernels address the tile copy with 32-bit byte offsets).
+ * N, K <= 65536.  bf16 / fp16: at most 2^21 - 1 kept 32 x 32 tiles (the
+ * kernels address the tile copy with 32-bit byte offsets) and K <= 63424 (a
+ * group's walk, one entry per 32 reduction columns, must fit the kernel's LDS
+ * table); SHAPE otherwise.
  * Errors: INVALID_ARG, SHAPE, DTYPE, BLOCK, ALLOC, HIP.
  */
 lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
@@ -177,7 +179,8 @@ lpv_status lpv_bsr_linear(const lpv_bsr* h, const void* X, int64_t ldx, int64_t 
  * K <= ldw <= 2^22), through the library's own matrix-core kernel: the
  * unpruned layer, the counterpart of the "Dense" rows of Tab. 2 and Tab. 4,
  * and the reference point for the speed-up of the block-sparse path.  Same
- * conventions as lpv_bsr_linear; N and K must be multiples of 16.
+ * conventions as lpv_bsr_linear; N and K must be multiples of 16 and at most
+ * 65536, K at most 63424 for bf16 / fp16 (SHAPE otherwise).
  */
 lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dtype dt,
                             const void* X, int64_t ldx, int64_t M, const void* bias, void* Y,

@@ -45,6 +45,10 @@ int elem_size(int dt)
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 constexpr int64_t MAX_DIM = 65536;  // N and K (schedule tables are sized for it)
+// K of the 16-bit kernels: one schedule group's walk (one 16-byte entry per
+// 32 reduction columns, padded to an even count) must fit the kernel's 32 KB
+// LDS table beside the group's descriptor and 1 KB of bias
+constexpr int64_t MAX_K16 = 63424;
 // Leading dimensions of X and W: the kernels address a 256-row tile of either
 // with 32-bit byte offsets.
 constexpr int64_t MAX_LD = (int64_t)1 << 22;
@@ -156,6 +160,9 @@ lpv_status lpv_bsr_pack(const void* W, int64_t ldw, int64_t N, int64_t K, lpv_dt
     if (N % b_r || K % b_c)
         return fail(LPV_ERR_SHAPE, "block %dx%d does not divide weight %lldx%lld", b_r, b_c,
                     (long long)N, (long long)K);
+    if (es == 2 && K > MAX_K16)
+        return fail(LPV_ERR_SHAPE, "K = %lld: the 16-bit kernels take K <= %lld", (long long)K,
+                    (long long)MAX_K16);
     if (!W || !mask)
         return fail(LPV_ERR_INVALID_ARG, "W and mask must not be NULL");
     if (ldw < K || (ldw * es) % 16 || !aligned16(W))
@@ -389,6 +396,9 @@ lpv_status lpv_dense_linear(const void* W, int64_t ldw, int64_t N, int64_t K, lp
     if (N <= 0 || K <= 0 || N > MAX_DIM || K > MAX_DIM || N % 16 || K % 16)
         return fail(LPV_ERR_SHAPE, "weight %lldx%lld: sides must be multiples of 16 in [16, %lld]",
                     (long long)N, (long long)K, (long long)MAX_DIM);
+    if (es == 2 && K > MAX_K16)
+        return fail(LPV_ERR_SHAPE, "K = %lld: the 16-bit kernels take K <= %lld", (long long)K,
+                    (long long)MAX_K16);
     if (!W || ldw < K || ldw > MAX_LD || (ldw * es) % 16 || !aligned16(W))
         return fail(LPV_ERR_INVALID_ARG, "W must be non-NULL, 16-byte aligned, K <= ldw <= 2^22 "
                                          "and ldw a multiple of 16 bytes");

@@ -69,6 +69,10 @@ def pack(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, b_r=32, b_c=32, mask=FAKE):
     (dict(N=1 << 17), SHAPE), (dict(K=-32), SHAPE),
     (dict(W=0), INVALID), (dict(mask=0), INVALID), (dict(W=FAKE + 8), INVALID),
     (dict(ldw=700), INVALID), (dict(ldw=772), INVALID),
+    # 16-bit types: K <= 63424 (a group's walk must fit the kernel's LDS table)
+    (dict(K=63456, ldw=63456), SHAPE), (dict(K=65536, ldw=65536, dt=1), SHAPE),
+    (dict(K=65536, ldw=65536, dt=0, W=0), INVALID),  # fp32 has no such limit
+    (dict(K=63424, ldw=63424, W=0), INVALID),        # the largest 16-bit K passes the shape checks
 ])
 def test_pack_rejects_bad_arguments(L, kw, want):
     assert pack(L, **kw) == want
@@ -98,6 +102,8 @@ def dense(L, W=FAKE, ldw=768, N=3072, K=768, dt=2, X=FAKE + (1 << 32), ldx=768, 
     (dict(Y=FAKE + (1 << 32) + 64), ALIAS), (dict(X=FAKE + (2 << 32) + 1024), ALIAS),
     # leading dimensions above 2^22 elements (32-bit byte offsets in the kernels)
     (dict(ldx=(1 << 22) + 8), INVALID), (dict(ldw=(1 << 22) + 8), INVALID),
+    # 16-bit types: K <= 63424
+    (dict(K=63440, ldw=63440, ldx=63440), SHAPE), (dict(K=65536, ldw=65536, ldx=65536, dt=1), SHAPE),
 ])
 def test_dense_rejects_bad_arguments(L, kw, want):
     assert dense(L, **kw) == want

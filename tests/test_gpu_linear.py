@@ -360,3 +360,17 @@ def test_full_b_stack_links_sampled():
         assert_close(f64(Y[rows_d]), r, "bf16", w.name + " sampled")
         h.close()
         X = Y
+
+
+@pytest.mark.parametrize("dense", [False, True])
+def test_largest_reduction(dense):
+    """K = 63424, the largest the 16-bit kernels take: one group's walk (1982
+    column tiles) fills the kernel's LDS table."""
+    w = wl.custom(80, 97, 256, 63424, 32, 32, "bf16", "uniform", 0 if dense else 50, gelu=True)
+    say("largest K", "dense" if dense else "sparse", "nnzb", w.nnzb)
+    if dense:
+        Y = lpv.dense_linear(dev(w.W, "bf16"), dev(w.X, "bf16"), dev(w.bias, "bf16"), epi="gelu")
+        torch.cuda.synchronize()
+    else:
+        _, Y = run_bsr(w)
+    assert_close(f64(Y), ref(w), "bf16", w.name)

@@ -78,3 +78,33 @@ def test_mask_feeds_pack_and_linear():
     err = oracle.rel_err(Y.float().cpu().numpy().astype(np.float64), r)
     say("  mask -> pack -> linear rel err %.3e" % err)
     assert err <= 2e-2
+
+
+def test_unaligned_weight_rows():
+    # row strides that are not multiples of 16 bytes (a view one element into
+    # a wider buffer): the scores take the kernel that reads element by element
+    for dtype in ("bf16", "f32"):
+        W = weights(65, 192, 256, dtype)
+        G = weights(66, 192, 256, dtype, scale=1.0)
+        say("mask_topk unaligned rows", dtype)
+        for taylor in (False, True):
+            buf = torch.zeros((192, 257), dtype=dev(W, dtype).dtype, device="cuda")
+            buf[:, 1:] = dev(W, dtype)
+            gbuf = torch.zeros_like(buf)
+            gbuf[:, 1:] = dev(G, dtype)
+            m_gpu, s_gpu = lpv.mask_topk(buf[:, 1:], 32, 32, 50, gbuf[:, 1:] if taylor else None)
+            torch.cuda.synchronize()
+            m_ref, s_ref = oracle.block_mask(W, dtype, 32, 32, 50, G if taylor else None)
+            assert np.array_equal(s_gpu.cpu().numpy().view(np.uint64), s_ref.view(np.uint64))
+            assert np.array_equal(m_gpu.cpu().numpy(), m_ref)
+
+
+def test_many_blocks_with_ties():
+    # 12288 blocks (more keys than the selection keeps in registers) of small
+    # integers, so many block scores are equal: ties still go to the lower index
+    g = np.random.default_rng(67)
+    Wi = g.integers(-2, 3, (2048, 1536)).astype(np.float32)
+    for p in (25, 50, 90):
+        check(Wi, "f32", 16, 16, p, what="12288 integer blocks")
+    Gi = g.integers(-2, 3, (2048, 1536)).astype(np.float32)
+    check(Wi.astype(np.float16), "f16", 16, 16, 50, Gi.astype(np.float16), what="12288 taylor")
