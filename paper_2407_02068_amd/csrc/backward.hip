@@ -13,6 +13,8 @@
 // Every sum is taken in a fixed order, so results do not depend on timing.
 #include <mutex>
 
+#include <type_traits>
+
 #include "lpv_device.h"
 #include "lpv_internal.h"
 
@@ -326,14 +328,17 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
         if (rank == my_rank)
             tj = j;
     }
-    const uint32_t rowbits = (uint32_t)(wmask >> (8 * tj)) & 0xffu;
-    const int n_w = __popc(rowbits);
+    // (wave-uniform values, kept in scalar registers: every per-tile test
+    // below is then one scalar compare and branch, not a lane mask)
+    tj = __builtin_amdgcn_readfirstlane(tj);
+    const uint32_t rowbits = __builtin_amdgcn_readfirstlane((uint32_t)(wmask >> (8 * tj)) & 0xffu);
+    const int n_w = __builtin_amdgcn_readfirstlane(__popc(rowbits));
     int tc[8];  // the row's kept tile columns, ascending
     {
         uint32_t rest = rowbits;
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-            tc[t] = rest ? __builtin_ctz(rest) : 0;
+            tc[t] = __builtin_amdgcn_readfirstlane(rest ? __builtin_ctz(rest) : 0);
             rest &= rest - 1;
         }
     }
@@ -396,29 +401,43 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
 
     // prologue: step 0
     dma_step(0);
-    for (int64_t st = 0; st < n_steps; ++st) {
-        // step st's DMA (the wave's only one in flight) has landed; the
-        // barrier publishes it to everyone and frees the stage of step st - 1,
-        // which then receives step st + 1
-        asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory");
-        if (st + 1 < n_steps)
-            dma_step(st + 1);
-        const uint32_t stage = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE;
+    // the token steps, with the row's kept-tile count NW a compile-time
+    // constant (one copy of the loop per count): no per-tile test in the loop
+    auto steps = [&](auto nw_c) {
+        constexpr int NW = decltype(nw_c)::value;
+        for (int64_t st = 0; st < n_steps; ++st) {
+            // step st's DMA (the wave's only one in flight) has landed; the
+            // barrier publishes it to everyone and frees the stage of step
+            // st - 1, which then receives step st + 1
+            asm volatile("s_waitcnt vmcnt(0)\n s_barrier" ::: "memory");
+            if (st + 1 < n_steps)
+                dma_step(st + 1);
+            const uint32_t stage = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE;
 #pragma unroll
-        for (int ks = 0; ks < GW_KS; ++ks) {
-            // one G fragment for the row, one X fragment per kept tile, each
-            // in registers of its own; then the products
-            const F a = frag(stage, ks, tj);
-            F b[8];
+            for (int ks = 0; ks < GW_KS; ++ks) {
+                // one G fragment for the row, one X fragment per kept tile,
+                // each in registers of its own; then the products
+                const F a = frag(stage, ks, tj);
+                F b[NW > 0 ? NW : 1];
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-                if (t < n_w)
+                for (int t = 0; t < NW; ++t)
                     b[t] = frag(stage + GW_XOFF, ks, tc[t]);
 #pragma unroll
-            for (int t = 0; t < 8; ++t)
-                if (t < n_w)
+                for (int t = 0; t < NW; ++t)
                     acc[t] = E::mma(a, b[t], acc[t]);
+            }
         }
+    };
+    switch (n_w) {
+    case 0: steps(std::integral_constant<int, 0>{}); break;
+    case 1: steps(std::integral_constant<int, 1>{}); break;
+    case 2: steps(std::integral_constant<int, 2>{}); break;
+    case 3: steps(std::integral_constant<int, 3>{}); break;
+    case 4: steps(std::integral_constant<int, 4>{}); break;
+    case 5: steps(std::integral_constant<int, 5>{}); break;
+    case 6: steps(std::integral_constant<int, 6>{}); break;
+    case 7: steps(std::integral_constant<int, 7>{}); break;
+    default: steps(std::integral_constant<int, 8>{}); break;
     }
 
     // partials of this chunk
