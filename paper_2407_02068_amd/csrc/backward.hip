@@ -654,7 +654,7 @@ hipError_t launch_grad_w(const lpv_bsr* h, const GradWCall& c, hipStream_t s)
     d.n_groups = h->n_groups;
     d.n_wcols = (h->n_tile_cols + 7) / 8;
     const int64_t n_win = (int64_t)d.n_groups * d.n_wcols;
-    // about one workgroup per compute unit; chunks of whole 32-token steps
+    // about one workgroup per compute unit; chunks of whole token steps
     int64_t n_chunks = grad_w_chunk_cap(h);
     n_chunks = min(n_chunks, (c.M + GW_TOK - 1) / GW_TOK);
     d.chunk_rows = ((c.M + n_chunks - 1) / n_chunks + GW_TOK - 1) / GW_TOK * GW_TOK;

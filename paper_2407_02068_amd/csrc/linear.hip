@@ -373,6 +373,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         uint32_t xcol, woff;
     };
     bool x_stale = false;  // the item advanced: set_x() before the next step
+    int p_rows = n_full == 0 ? 0xf << (4 * hh) : 0xff;  // rows the producer's item keeps
     auto p_prepare = [&](int slot, Dma& d) -> int {
         // (the previous step's DMA, issued after its p_prepare, used the old
         // item's bases)
@@ -391,7 +392,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         const int col = ex & 0xffff, all_bits = (ex >> 16) & 0xff;
         // a half item keeps its own half's rows (the tile stream order, and so
         // a tile's rank, still counts every kept row of the step)
-        const int bits = pk == n_full ? all_bits & (0xf << (4 * hh)) : all_bits;
+        const int bits = all_bits & p_rows;
         d.col = col;
         d.xcol = (uint32_t)col * (TILE * 2);
         d.n = bits ? 2 : 0;  // a step that keeps no tile (walk padding) loads nothing
@@ -417,6 +418,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         if ((ex & W_LAST) && ++pk < my_items) {
             if (pk == n_full) {
                 // on to the half item: its walk replaces the prefetched one
+                p_rows = 0xf << (4 * hh);
                 p_slot = h_slot;
                 p_mt = h_mt;
                 cur = seg_read(t_desc[h_slot].y);
