@@ -685,6 +685,11 @@ def time_stack(steps, to_dev, power=True):
     _, lms = time_launches(lambda: lpv.add_layernorm(R[0], P, g1, b0, 1e-6, S=R[1], out=A),
                            max(10, steps // 2), 5)
     pw = measure_power(sparse, dense, unit="256_images") if power else None
+    # the same chains captured into HIP graphs (one replay = one forward pass)
+    g_s, _ = chain.capture(X0, sparse=True)
+    g_d, _ = chain.capture(X0, sparse=False)
+    gms, gdms = interleaved(g_s.replay, g_d.replay, 3, n)
+    del g_s, g_d
     chain.close()
     kept = sum(w.kept_flops() for w in layers)
     dense_fl = sum(w.dense_flops() for w in layers)
@@ -695,6 +700,8 @@ def time_stack(steps, to_dev, power=True):
             "kept_gflop": round(kept / 1e9, 1), "dense_gflop": round(dense_fl / 1e9, 1),
             "ms": round(avg(sms), 4), "images_per_s": round(n_seq / (avg(sms) * 1e-3), 1),
             "dense_ms": round(avg(dms), 4), "speedup_vs_dense": round(avg(dms) / avg(sms), 3),
+            "graph_ms": round(avg(gms), 4), "graph_dense_ms": round(avg(gdms), 4),
+            "graph_images_per_s": round(n_seq / (avg(gms) * 1e-3), 1),
             "linear_ms": round(lin_s, 4), "linear_dense_ms": round(lin_d, 4),
             "linear_tflops": round(kept / (lin_s * 1e-3) / 1e12, 1),
             "linear_speedup_vs_dense": round(lin_d / lin_s, 3),
@@ -706,8 +713,9 @@ def time_stack(steps, to_dev, power=True):
             "note": "event averages of the whole encoder (12 blocks, 25 LN, 12 attention, 48 "
                     "linear launches), block-sparse and dense chains interleaved; linear_ms = the "
                     "48 linear launches' event times inside the chain (linear_tflops = kept "
-                    "FLOPs / linear_ms); DeiT-B, 256 x 197 tokens, 32x32 blocks; attention and "
-                    "LN timed alone at the same shape"}
+                    "FLOPs / linear_ms); graph_ms / graph_dense_ms: the same chains captured "
+                    "once into HIP graphs and replayed; DeiT-B, 256 x 197 tokens, 32x32 blocks; "
+                    "attention and LN timed alone at the same shape"}
 
 
 def sweep(steps, cfgs=("fc1", "s_fc1", "b_layer")):
@@ -981,6 +989,8 @@ def main():
                stack["linear_ms"], stack["linear_dense_ms"], stack["linear_tflops"],
                stack["attention_ms"] * 1e3, stack["attention_tflops"],
                stack["add_layernorm_ms"] * 1e3, stack["add_layernorm_GBs"]))
+        log("DeiT-B encoder as HIP graph replays: %.2f ms (%.0f images/s), dense linears %.2f ms"
+            % (stack["graph_ms"], stack["graph_images_per_s"], stack["graph_dense_ms"]))
         if stack.get("power"):
             log("encoder power: %s" % json.dumps(stack["power"]))
     if dcurve:

@@ -185,3 +185,31 @@ def test_encoder_chain_batch4_in_full():
 
 def test_encoder_chain_batch256_sampled():
     _check_chain(256, 1, (0, 77, 255))
+
+
+@pytest.mark.parametrize("sparse", [True, False])
+def test_encoder_chain_graph_replays(sparse):
+    """The chain captured into a HIP graph: three replays, each after eager work
+    that overwrites the outputs (and a synchronisation), give the eager pass's
+    result bit for bit."""
+    T, H = 197, 12
+    layers = wl.b_stack(M=4 * T, layers=2)
+    chain = deit_chain(layers, lambda a: dev(a, "bf16"), 4, T, H)
+    x0 = dev(layers[0].X, "bf16")
+    say("encoder graph", "block-sparse" if sparse else "dense", "4 sequences, 2 blocks")
+    x, A = chain.run(x0, sparse=sparse)
+    torch.cuda.synchronize()
+    x_ref, A_ref = x.clone(), A.clone()
+    graph, (xg, Ag) = chain.capture(x0, sparse=sparse)
+    assert xg.data_ptr() == x.data_ptr() and Ag.data_ptr() == A.data_ptr()
+    for i in range(3):
+        # eager work between replays: the other path's forward, then the outputs cleared
+        chain.run(x0, sparse=not sparse)
+        xg.zero_()
+        Ag.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(xg.view(torch.int16), x_ref.view(torch.int16)), "replay %d: x" % i
+        assert torch.equal(Ag.view(torch.int16), A_ref.view(torch.int16)), "replay %d: A" % i
+    chain.close()
