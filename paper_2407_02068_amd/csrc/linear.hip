@@ -6,7 +6,9 @@
 // An item walks its group's steps -- the 32-wide reduction columns where any
 // of its rows keeps a tile; other columns are never touched -- so its work is
 // proportional to the kept tiles, the quantity the paper's cost model counts
-// (Sec. 3.4).  The walk starts at a per-group column and wraps around, so the
+// (Sec. 3.4); with 16-wide block columns (KH) the two 16-column halves of a
+// tile are kept or dropped on their own, and only kept halves are loaded and
+// multiplied.  The walk starts at a per-group column and wraps around, so the
 // groups that work on one token tile at the same time read different X
 // columns.
 //
@@ -163,7 +165,10 @@ __device__ inline int xswz(int r) { return (r >> 1) & 7; }
 
 // Walk entry (LDS table): {col | bits << 16 | last step of the item << 24 |
 // last entry of its segment << 25, first tile, start of the next segment in
-// this grid's item order, group}.  A slot's walk is cut into segments of at
+// this grid's item order, group}.  With 16-wide block columns (KH) a kept
+// tile's two 16-column halves are kept or dropped on their own: bits are then
+// the rows that keep the first half, and the first-tile word carries the rows
+// that keep the second half in its top byte.  A slot's walk is cut into segments of at
 // most 64 entries; the producer holds one segment in VGPR lanes (lane i =
 // entry i) and the next one prefetched, so a step costs two lane reads and no
 // memory access.
@@ -174,12 +179,13 @@ constexpr int SEG = 64;
 // the last item are 0).
 constexpr int E_LAST = 1 << 8, E_VALID = 1 << 9, E_BITS = 12, E_MASK = (1 << E_BITS) - 1;
 
-template <int DT, bool GELU, bool DENSE, bool KTAIL>
+template <int DT, bool GELU, bool DENSE, bool KTAIL, bool KH>
 __global__ __launch_bounds__(NT, 1) void k_linear16(
     const Dims a, const char* __restrict__ X, const char* __restrict__ stream,
     const int4* __restrict__ gdesc, const int2* __restrict__ walk,
     const char* __restrict__ W, const char* __restrict__ bias, char* __restrict__ Y)
 {
+    static_assert(!(DENSE && KH), "the dense path keeps whole tiles");
     using E = Elem<DT>;
     using F = typename E::frag;
     __shared__ uint4 smem[2 * PSLOT + TAB_U4];
@@ -368,8 +374,11 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // for a step that keeps no tile, 2 with X only, 4 with this wave's W
     // tile), the column tile and its byte offset in a row of X / dense W, and
     // (sparse) the byte offset of this wave's W tile in the tile stream.
+    // KH: the halves of this wave's tile to load (hl: bit 0 the first 16
+    // columns, bit 1 the second) and the step's rows that keep the second
+    // half (hq, for the consumer).
     struct Dma {
-        int slot, n, col;
+        int slot, n, col, hl, hq;
         uint32_t xcol, woff;
     };
     bool x_stale = false;  // the item advanced: set_x() before the next step
@@ -384,12 +393,22 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         d.slot = slot;
         d.n = 0;
         d.col = 0;
+        d.hl = 0;
+        d.hq = 0;
         d.xcol = 0;
         d.woff = 0;
         if (pk >= my_items)
             return 0;
         const int ex = __builtin_amdgcn_readlane(cur.x, p_i);
-        const int col = ex & 0xffff, all_bits = (ex >> 16) & 0xff;
+        const int col = ex & 0xffff;
+        int lo_bits = (ex >> 16) & 0xff, hi_bits = lo_bits, all_bits = lo_bits;
+        int tile0 = 0;
+        if (KH) {
+            const int ey = __builtin_amdgcn_readlane(cur.y, p_i);
+            hi_bits = (int)((uint32_t)ey >> 24);
+            all_bits = lo_bits | hi_bits;
+            tile0 = ey & 0xffffff;
+        }
         // a half item keeps its own half's rows (the tile stream order, and so
         // a tile's rank, still counts every kept row of the step)
         const int bits = all_bits & p_rows;
@@ -402,10 +421,14 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         } else if ((bits >> wave) & 1) {  // row `wave` of the group is kept: its tile
             // (the stream holds fewer than 2^21 tiles: the offset fits 32 bits)
             const int rank = __popc(all_bits & ((1 << wave) - 1));
-            d.woff = (uint32_t)(__builtin_amdgcn_readlane(cur.y, p_i) + rank) * 2048u;
+            d.woff = (uint32_t)((KH ? tile0 : __builtin_amdgcn_readlane(cur.y, p_i)) + rank) * 2048u;
             d.n = 4;
+            if (KH)
+                d.hl = ((lo_bits >> wave) & 1) | (((hi_bits >> wave) & 1) << 1);
         }
-        const int e = bits | ((ex & W_LAST) ? E_LAST : 0) | E_VALID;
+        if (KH)
+            d.hq = hi_bits & p_rows;
+        const int e = (KH ? lo_bits & p_rows : bits) | ((ex & W_LAST) ? E_LAST : 0) | E_VALID;
         // advance: next entry of the segment, or the next segment (whose
         // successor is read now; every half step waits for LDS reads)
         if (ex & W_SEG_END) {
@@ -497,25 +520,34 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             dma16i<2048>(wibase - 2048, wioff[2] + vo[2], mw);
             dma16i<3072>(wibase - 3072, wioff[3] + vo[3], mw);
         } else {
+            // (KH: only the kept halves; a dropped half's LDS keeps stale data
+            // that no matrix-core instruction reads)
             if (d0.n == 4) {
                 const uint32_t mw = wa + (uint32_t)wave * 2048;
-                dma16i<0>(stream, loff + d0.woff, mw);
-                dma16i<1024>(stream, loff + d0.woff, mw);
+                if (!KH || (d0.hl & 1))
+                    dma16i<0>(stream, loff + d0.woff, mw);
+                if (!KH || (d0.hl & 2))
+                    dma16i<1024>(stream, loff + d0.woff, mw);
             }
             if (d1.n == 4) {
                 const uint32_t mw = wa + WS_U4 * 16 + (uint32_t)wave * 2048;
-                dma16i<0>(stream, loff + d1.woff, mw);
-                dma16i<1024>(stream, loff + d1.woff, mw);
+                if (!KH || (d1.hl & 1))
+                    dma16i<0>(stream, loff + d1.woff, mw);
+                if (!KH || (d1.hl & 2))
+                    dma16i<1024>(stream, loff + d1.woff, mw);
             }
         }
     };
 
     // ---- prologue: the first pair of steps
     uint64_t q = 0;  // queue entries of steps t, t + 1, ... (E_BITS each)
+    uint32_t qh = 0;  // KH: their second-half row bits, 8 each
     {
         Dma d0, d1;
         q |= (uint64_t)(uint32_t)p_prepare(0, d0);
         q |= (uint64_t)(uint32_t)p_prepare(1, d1) << E_BITS;
+        if (KH)
+            qh |= (uint32_t)d0.hq | (uint32_t)d1.hq << 8;
         dma_x(d0, d1);
         dma_w(d0, d1);
     }
@@ -752,6 +784,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             Dma d0, d1;
             q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
             q |= (uint64_t)(uint32_t)p_prepare((t + 3) & (NS - 1), d1) << (3 * E_BITS);
+            if (KH)
+                qh |= (uint32_t)d0.hq << 16 | (uint32_t)d1.hq << 24;
             dma_x(d0, d1);
             if (have)
                 flush(((t + 2) >> 1) & 1);
@@ -760,11 +794,15 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         init_acc(c_slot);
         for (;;) {  // the pairs of the item
             const int e0 = (int)(q & E_MASK), e1 = (int)((q >> E_BITS) & E_MASK);
+            // rows of each step that keep the second k-step (KH: their own bits)
+            const int h0 = KH ? (int)(qh & 0xff) : e0 & 0xff;
+            const int h1 = KH ? (int)((qh >> 8) & 0xff) : e1 & 0xff;
             half_a(t, e0 & 0xff);
-            half_b(t, e0 & 0xff, true);
+            half_b(t, h0, true);
             half_a(t + 1, e1 & 0xff);
-            half_b(t + 1, e1 & 0xff, false);
+            half_b(t + 1, h1, false);
             q >>= 2 * E_BITS;
+            qh >>= 16;
             t += 2;
             sync();
             if (e1 & E_LAST)
@@ -773,6 +811,8 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             Dma d0, d1;
             q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
             q |= (uint64_t)(uint32_t)p_prepare((t + 3) & (NS - 1), d1) << (3 * E_BITS);
+            if (KH)
+                qh |= (uint32_t)d0.hq << 16 | (uint32_t)d1.hq << 24;
             dma_x(d0, d1);
             dma_w(d0, d1);
         }
@@ -868,6 +908,7 @@ struct Args {
     const char* W;            // dense weight
     const char* bias;
     char* Y;
+    bool kh;                  // sparse, 16-wide block columns: tile halves walked on their own
 };
 
 template <bool DENSE>
@@ -875,6 +916,8 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
 {
     const int64_t n_mt = (a.d.M + BM - 1) / BM;
     const bool ktail = (a.d.K % TILE) != 0;
+    if (!DENSE && ktail && !a.kh)
+        return hipErrorInvalidValue;  // (a block width of 32 or 64 divides K into whole tiles)
     const int P0 = max(num_cus() & ~7, 8);
     // Launches over consecutive launch slots whose tables fit the 32 KB of LDS
     // reserved for them: 16 B per slot descriptor and walk entry, 1 KB of float32 bias
@@ -922,15 +965,26 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
             d.mt_carry = 1;
         }
         const dim3 grid(P), block(NT);
-#define LPV_LAUNCH1(DT_, GELU_, KT_)                                                              \
-    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_>), grid, block, 0, s, d, a.X, a.stream, \
-                       a.gdesc, a.walk, a.W, a.bias, a.Y)
+#define LPV_LAUNCH1(DT_, GELU_, KT_, KH_)                                                         \
+    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_, KH_>), grid, block, 0, s, d, a.X,      \
+                       a.stream, a.gdesc, a.walk, a.W, a.bias, a.Y)
+        // A reduction tail (K = 16 mod 32) only occurs with 16-wide block
+        // columns, so the sparse tail kernels are the KH ones.
 #define LPV_LAUNCH(DT_, GELU_)                                                                    \
     do {                                                                                          \
-        if (ktail)                                                                                \
-            LPV_LAUNCH1(DT_, GELU_, true);                                                        \
-        else                                                                                      \
-            LPV_LAUNCH1(DT_, GELU_, false);                                                       \
+        if constexpr (DENSE) {                                                                    \
+            if (ktail)                                                                            \
+                LPV_LAUNCH1(DT_, GELU_, true, false);                                             \
+            else                                                                                  \
+                LPV_LAUNCH1(DT_, GELU_, false, false);                                            \
+        } else {                                                                                  \
+            if (!a.kh)                                                                            \
+                LPV_LAUNCH1(DT_, GELU_, false, false);                                            \
+            else if (ktail)                                                                       \
+                LPV_LAUNCH1(DT_, GELU_, true, true);                                              \
+            else                                                                                  \
+                LPV_LAUNCH1(DT_, GELU_, false, true);                                             \
+        }                                                                                         \
     } while (0)
         if (dtype == LPV_BF16) {
             if (gelu)
@@ -1001,6 +1055,7 @@ hipError_t launch_bsr_linear(const lpv_bsr* h, const LinearCall& c, hipStream_t 
     a.gdesc = h->gdesc;
     a.gdesc_host = h->gdesc_host;
     a.walk = h->walk;
+    a.kh = h->b_c == 16;
     return launch16<false>(h->dtype, c.gelu != 0, a, s);
 }
 

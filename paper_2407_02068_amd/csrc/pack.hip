@@ -287,10 +287,33 @@ __global__ __launch_bounds__(256) void k_stream_fill(PackArgs a, const int32_t* 
     }
 }
 
+// Rows of group g whose tile at column tc keeps a block in the tile's 16-column
+// half h (16-wide block columns: that half is block column 2 tc + h).
+__device__ inline int half_bits(const PackArgs& a, int g, int tc, int h)
+{
+    const int c = 2 * tc + h;
+    if (c >= a.C)
+        return 0;
+    int bits = 0;
+    for (int j = 0; j < GROUP_TILES; ++j) {
+        const int tr = g * GROUP_TILES + j;
+        if (tr >= a.n_tile_rows)
+            break;
+        const int r0 = tr * TILE / a.b_r, r1 = min((tr * TILE + TILE - 1) / a.b_r, a.R - 1);
+        for (int r = r0; r <= r1; ++r)
+            if (a.mask[(int64_t)r * a.C + c] != 0)
+                bits |= 1 << j;
+    }
+    return bits;
+}
+
 // One wave per launch slot: the slot's walk, the group's steps starting at its
 // rotation and wrapping, as {col | bits << 16 | last << 24, first tile}, then
-// steps with no tile up to the (even) walk length.
-__global__ __launch_bounds__(64) void k_walk_fill(const int4* __restrict__ gdesc,
+// steps with no tile up to the (even) walk length.  With 16-wide block columns
+// bits are the rows that keep the tile's first 16 columns, and the rows that
+// keep its second 16 go in the top byte of the first-tile word (fewer than
+// 2^21 tiles), so that the linear kernel moves and multiplies only kept halves.
+__global__ __launch_bounds__(64) void k_walk_fill(const PackArgs a, const int4* __restrict__ gdesc,
                                                   const int32_t* __restrict__ step_ptr,
                                                   const int32_t* __restrict__ step_col,
                                                   const int32_t* __restrict__ step_bits,
@@ -307,7 +330,13 @@ __global__ __launch_bounds__(64) void k_walk_fill(const int4* __restrict__ gdesc
             if (j >= ns)
                 j -= ns;
             const int s = s0 + j;
-            e = make_int2(step_col[s] | (step_bits[s] << 16) | last, step_tile[s]);
+            if (a.b_c == 16) {
+                const int tc = step_col[s];
+                e = make_int2(tc | (half_bits(a, d.x, tc, 0) << 16) | last,
+                              step_tile[s] | (half_bits(a, d.x, tc, 1) << 24));
+            } else {
+                e = make_int2(step_col[s] | (step_bits[s] << 16) | last, step_tile[s]);
+            }
         }
         walk[d.y + i] = e;
     }
@@ -376,7 +405,7 @@ hipError_t launch_pack_fill(const PackArgs& a, const lpv_bsr* h, hipStream_t s)
                            h->step_ptr, h->step_col, h->step_bits, h->step_tile,
                            (uint4*)h->stream_vals);
     if (a.n_groups > 0)
-        hipLaunchKernelGGL(k_walk_fill, dim3(a.n_groups), dim3(64), 0, s, h->gdesc, h->step_ptr,
+        hipLaunchKernelGGL(k_walk_fill, dim3(a.n_groups), dim3(64), 0, s, a, h->gdesc, h->step_ptr,
                            h->step_col, h->step_bits, h->step_tile, h->walk);
     return hipGetLastError();
 }

@@ -255,6 +255,58 @@ def test_chain_b_stack_links():
         X = Y
 
 
+# ---- 16-wide block columns: tiles walked by 16-column halves -------------------
+
+def _half_mask(g, R, C, pattern):
+    """Block masks over 16-wide block columns: kept blocks only in even block
+    columns (every kept tile keeps its first 16 columns only), only in odd
+    ones (second half only), or anywhere (all three kinds of kept tile)."""
+    keep = g.random((R, C)) < (0.6 if pattern != "random" else 0.35)
+    if pattern == "first":
+        keep[:, 1::2] = False
+    elif pattern == "second":
+        keep[:, 0::2] = False
+    return keep.astype(np.uint8)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+@pytest.mark.parametrize("b_r", [16, 32])
+@pytest.mark.parametrize("pattern", ["first", "second", "random"])
+def test_half_kept_tiles(dtype, b_r, pattern):
+    """16-wide block columns: a kept 32 x 32 tile may keep one 16-column half
+    and drop the other, and the kernel then moves and multiplies the kept half
+    only.  Integer inputs (exact in every order), K = 336 (a 16-column tail),
+    M = 300, two output groups; the result must equal the oracle's bit for bit."""
+    g = np.random.default_rng(90 + b_r + len(pattern))
+    M, N, K = 300, 384, 336
+    Xf = g.integers(-1, 2, size=(M, K)) * (g.random((M, K)) < 0.2)
+    Wf = g.integers(-2, 3, size=(N, K))
+    bf = g.integers(-8, 9, size=N)
+    mask = _half_mask(g, N // b_r, K // 16, pattern)
+    w = wl.Linear("half." + pattern, dtype, b_r, 16, wl.quantize(Wf, dtype), mask,
+                  wl.quantize(bf, dtype), False, wl.quantize(Xf, dtype), M)
+    r = ref(w)
+    assert np.max(np.abs(r)) < 256  # exact in bf16
+    say("half tiles", dtype, b_r, pattern, "nnzb", int(mask.sum()))
+    _, Y = run_bsr(w)
+    assert np.array_equal(f64(Y), r)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f16"])
+def test_whole_tiles_as_16x16_blocks(dtype):
+    """A 32 x 32 block mask written as 16 x 16 blocks (each kept block as its
+    four quarters) keeps the same tiles with both halves: the two handles must
+    give the same output bits (GELU on, M = 300, DeiT-S fc1 shape)."""
+    w = wl.custom(92, 300, 1536, 384, 32, 32, dtype, "uniform", 50, gelu=True)
+    _, Y32 = run_bsr(w)
+    w16 = wl.Linear(w.name + ".as16", dtype, 16, 16, w.W, np.kron(w.mask, np.ones((2, 2), np.uint8)),
+                    w.bias, True, w.X, w.M)
+    _, Y16 = run_bsr(w16)
+    say("whole tiles as 16x16", dtype)
+    assert torch.equal(Y32.view(torch.int16), Y16.view(torch.int16))
+    assert_close(f64(Y16), ref(w), dtype, w16.name)
+
+
 # ---- shapes and paths the headline shapes never reach ----------------------------
 
 TAIL_SHAPES = ((80, 48, 16, 16), (48, 80, 16, 16), (208, 112, 16, 16), (80, 64, 16, 32),
@@ -307,15 +359,17 @@ def test_multi_launch_tables(N, K):
     assert_close(f64(Yd), r, "bf16", "dense " + w.name)
 
 
-@pytest.mark.parametrize("dense", [False, True])
-def test_last_round_split(dense):
+@pytest.mark.parametrize("dense,block", [(False, 32), (False, 16), (True, 32)])
+def test_last_round_split(dense, block):
     """38 token tiles x 12 output groups: with 256 compute units, 8 XCDs of 32
     workgroups, XCDs 0-5 own 5 token tiles (60 items: one whole round of 32
     and 28 left, too many to halve) and XCDs 6-7 own 4 (48 items: 16 left,
     each run as two half items).  Rows of tiles on both kinds of XCD are
-    checked against the oracle, for the block-sparse and the dense launch."""
-    w = wl.custom(78, 38 * 256, 3072, 768, 32, 32, "bf16", "uniform", 0 if dense else 50)
-    say("last round split", "dense" if dense else "sparse", "M", w.M, "nnzb", w.nnzb)
+    checked against the oracle, for the block-sparse launch (32 x 32 blocks,
+    and 16 x 16 blocks, whose tiles are walked by 16-column halves) and the
+    dense one."""
+    w = wl.custom(78, 38 * 256, 3072, 768, block, block, "bf16", "uniform", 0 if dense else 50)
+    say("last round split", "dense" if dense else "sparse", block, "M", w.M, "nnzb", w.nnzb)
     if dense:
         Y = lpv.dense_linear(dev(w.W, "bf16"), dev(w.X, "bf16"), dev(w.bias, "bf16"))
         torch.cuda.synchronize()
