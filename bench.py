@@ -66,8 +66,8 @@ def algorithmic_bytes(M, N, K, nnzb, b_r, b_c, kused_cols, es=2):
     return es * (M * kused_cols + M * N + nnzb * b_r * b_c + N) + 4 * (N // b_r + 1 + nnzb)
 
 
-SPARSE_KERNEL = "k_linear16<2, false, false"   # bf16, no GELU, block-sparse (demangled prefix)
-DENSE_KERNEL = "k_linear16<2, false, true"     # bf16, no GELU, dense
+SPARSE_KERNEL = "k_linear16<2, false, false, false, false>"  # bf16, no GELU, block-sparse, 32-wide blocks
+DENSE_KERNEL = "k_linear16<2, false, true, false, false>"    # bf16, no GELU, dense
 CALIB_BYTES = 1 << 30                        # the calibration copy reads and writes this much
 
 
@@ -114,12 +114,13 @@ def write_traffic(fetch_csv, write_csv, command):
 def kernel_label(name):
     """A short name for a kernel of the rocprofv3 statistics."""
     import re
-    m = re.search(r"k_linear16<(\d), (true|false), (true|false), (true|false)>", name)
+    m = re.search(r"k_linear16<(\d), (true|false), (true|false), (true|false), (true|false)>", name)
     if m:
-        return "k_linear16 %s %s%s%s (%s)" % (
+        return "k_linear16 %s %s%s%s%s (%s)" % (
             {"2": "bf16", "1": "fp16"}[m.group(1)],
             "dense" if m.group(3) == "true" else "block-sparse",
             " + GELU" if m.group(2) == "true" else "", ", K tail" if m.group(4) == "true" else "",
+            ", 16-column halves" if m.group(5) == "true" else "",
             "lpv_dense_linear" if m.group(3) == "true" else "lpv_bsr_linear")
     labels = (("k_block_scores_lds<2, true", "k_block_scores_lds, Taylor (lpv_delta_curve)"),
               ("k_block_scores_lds<2, false", "k_block_scores_lds, sum of squares (lpv_mask_topk)"),
@@ -127,8 +128,7 @@ def kernel_label(name):
               ("k_block_scores<2, false", "k_block_scores, sum of squares (lpv_mask_topk)"),
               ("k_block_scores", "k_block_scores (lpv_mask_topk)"),
               ("k_delta_dots", "k_delta_dots (lpv_delta_curve)"),
-              ("k_rank_counts", "k_rank_counts (lpv_delta_curve)"),
-              ("k_rank_scatter", "k_rank_scatter (lpv_delta_curve)"),
+              ("k_rank", "k_rank (lpv_delta_curve)"),
               ("k_delta_steps", "k_delta_steps (lpv_delta_curve)"),
               ("k_delta_finish", "k_delta_finish (lpv_delta_curve)"),
               ("k_mask_topk", "k_mask_topk (lpv_mask_topk)"),
@@ -217,7 +217,7 @@ def write_stats(stats_csv, command, backward=False, trace_csv=None, bench_log=No
         text += ["", "The block-sparse k_linear16 row counts the forward launches and the dX "
                  "launches (the same kernel on the transposed handle).  dW is k_gradw_tiles + "
                  "k_gradw_reduce, db k_bias_partial + k_bias_reduce, the delta curve "
-                 "k_block_scores_lds + k_rank_counts + k_rank_scatter + k_delta_dots + "
+                 "k_block_scores_lds + k_rank + k_delta_dots + "
                  "k_delta_steps + k_delta_finish; Cijk_Ailk is hipBLASLt's dense G^T X "
                  "reference, Custom_Cijk_Alik its dense forward."]
     else:

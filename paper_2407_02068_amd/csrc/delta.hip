@@ -13,8 +13,7 @@
 // (per-sample gradients, grad, and W itself for |d|^2) with -W over every
 // block: one pass over the per-sample gradients, which bounds the time (HBM).
 //
-//   k_rank_counts, k_rank_scatter
-//                  rank of each block by (-score, index) and its inverse
+//   k_rank         rank of each block by (-score, index) and its inverse
 //   k_delta_dots   float64 block dot products, one workgroup per (block-row,
 //                  vector)
 //   k_delta_steps  each vector's sum over each ratio step's blocks
@@ -28,41 +27,38 @@ namespace {
 
 // rank[b] = #{b' : score(b') > score(b), or equal and b' < b}; perm[rank[b]] = b.
 // Scores are non-negative, so their bit patterns order like their values.
-// k_rank_counts: thread b, chunk j of `chunk` keys (staged in LDS): the count
-// of that chunk's keys ahead of b, to cnt[j][b].  k_rank_scatter adds the
-// chunks' counts (integers: exact in any order) and writes perm.
-__global__ __launch_bounds__(256) void k_rank_counts(const double* __restrict__ scores, int64_t nb,
-                                                     int32_t chunk, int32_t* __restrict__ cnt)
-{
-    extern __shared__ uint64_t s_key[];
-    const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    const int64_t base = (int64_t)blockIdx.y * chunk;
-    const int n = (int)min((int64_t)chunk, nb - base);
-    for (int i = threadIdx.x; i < n; i += 256)
-        s_key[i] = (uint64_t)__double_as_longlong(scores[base + i]);
-    __syncthreads();
-    if (b >= nb)
-        return;
-    const uint64_t key = (uint64_t)__double_as_longlong(scores[b]);
-    int32_t r = 0;
-    for (int i = 0; i < n; ++i) {
-        const uint64_t k2 = s_key[i];
-        r += (k2 > key) || (k2 == key && base + i < b);
-    }
-    cnt[(int64_t)blockIdx.y * nb + b] = r;
-}
+// Workgroup: 64 blocks (lane l: block 64 x + l) times RANK_WAVES waves; wave w
+// counts the keys ahead of its lane's block in the w-th part of the key range
+// (each key read once per wave, a wave-uniform load); the parts' integer
+// counts are added in LDS (exact in any order) and the permutation written.
+constexpr int RANK_WAVES = 16;
 
-__global__ __launch_bounds__(256) void k_rank_scatter(const int32_t* __restrict__ cnt, int64_t nb,
-                                                      int32_t n_chunks, int32_t* __restrict__ perm)
+__global__ __launch_bounds__(64 * RANK_WAVES) void k_rank(const double* __restrict__ scores,
+                                                          int64_t nb, int32_t* __restrict__ perm)
 {
-    const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (b >= nb)
-        return;
-    int64_t rank = 0;
+    __shared__ int32_t s_cnt[RANK_WAVES][64];
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane((int)(threadIdx.x >> 6));
+    const int64_t b = (int64_t)blockIdx.x * 64 + lane;
+    const uint64_t* keys = (const uint64_t*)scores;
+    const uint64_t key = keys[min(b, nb - 1)];
+    const int64_t per = (nb + RANK_WAVES - 1) / RANK_WAVES;
+    const int64_t k0 = min(nb, (int64_t)w * per), k1 = min(nb, k0 + per);
+    int32_t r = 0;
 #pragma unroll 8
-    for (int j = 0; j < n_chunks; ++j)
-        rank += cnt[(int64_t)j * nb + b];
-    perm[rank] = (int32_t)b;
+    for (int64_t i = k0; i < k1; ++i) {
+        const uint64_t k2 = keys[i];
+        r += (k2 > key) || (k2 == key && i < b);
+    }
+    s_cnt[w][lane] = r;
+    __syncthreads();
+    if (w == 0 && b < nb) {
+        int32_t rank = 0;
+#pragma unroll
+        for (int j = 0; j < RANK_WAVES; ++j)
+            rank += s_cnt[j][lane];
+        perm[rank] = (int32_t)b;
+    }
 }
 
 // The 8 elements at idx .. idx + 7 (idx a multiple of 8, 16-byte aligned) in
@@ -190,38 +186,51 @@ __global__ __launch_bounds__(256) void k_delta_steps(const DeltaCall c, int64_t 
 // One workgroup.  Sample v keeps a_v = g_v . dW_{k-1} and turns its step sums
 // into (B_k / 2 + a_v) B_k (in place); then thread k adds the samples' terms
 // in order; thread 0 adds, step by step, grad . d + kappa |d|^2 / 2 +
-// (1/N) sum_v (...).
+// (1/N) sum_v (...).  STAGED: the step sums and the step terms sit in LDS (one
+// coalesced load first), so none of the serial loops waits on global memory.
+template <bool STAGED>
 __global__ __launch_bounds__(1024) void k_delta_finish(const DeltaCall c, double* __restrict__ bsum,
                                                        double* __restrict__ term)
 {
+    extern __shared__ double s_fin[];  // STAGED: step sums (n_points x nv), step terms
     const int64_t nv = c.n_samples + 2;
+    double* q = bsum;
+    double* tk = term;
+    if (STAGED) {
+        const int64_t n = (int64_t)c.n_points * nv;
+        for (int64_t i = threadIdx.x; i < n; i += 1024)
+            s_fin[i] = bsum[i];
+        __syncthreads();
+        q = s_fin;
+        tk = s_fin + n;
+    }
     // (the loads of each loop are independent of its running sums: unrolled,
     // they are issued ahead of the additions)
     for (int64_t v = threadIdx.x; v < c.n_samples; v += 1024) {
         double a = 0.0;
 #pragma unroll 8
         for (int k = 0; k < c.n_points; ++k) {
-            const double b = bsum[(int64_t)k * nv + v];
-            bsum[(int64_t)k * nv + v] = (0.5 * b + a) * b;
+            const double b = q[(int64_t)k * nv + v];
+            q[(int64_t)k * nv + v] = (0.5 * b + a) * b;
             a += b;
         }
     }
     __syncthreads();
     for (int k = threadIdx.x; k < c.n_points; k += 1024) {
-        const double* qk = bsum + (int64_t)k * nv;
+        const double* qk = q + (int64_t)k * nv;
         double f = 0.0;
 #pragma unroll 16
         for (int64_t v = 0; v < c.n_samples; ++v)
             f += qk[v];
         // grad . d, and |d|^2 = -(W . (-W)) over the step
-        term[k] = qk[c.n_samples] + 0.5 * c.kappa * -qk[c.n_samples + 1] +
-                  (c.n_samples > 0 ? f / (double)c.n_samples : 0.0);
+        tk[k] = qk[c.n_samples] + 0.5 * c.kappa * -qk[c.n_samples + 1] +
+                (c.n_samples > 0 ? f / (double)c.n_samples : 0.0);
     }
     __syncthreads();
     if (threadIdx.x == 0) {
         double delta = 0.0;
         for (int k = 0; k < c.n_points; ++k) {
-            delta += term[k];
+            delta += tk[k];
             c.delta[k] = delta;
         }
     }
@@ -229,27 +238,20 @@ __global__ __launch_bounds__(1024) void k_delta_finish(const DeltaCall c, double
 
 }  // namespace
 
-// Ranking: keys in chunks of at least 128, at most 64 chunks.
-static int32_t rank_chunk(int64_t nb) { return (int32_t)max((int64_t)128, (nb + 63) / 64); }
-
 size_t delta_workspace_bytes(int64_t N, int64_t K, int32_t b_r, int32_t b_c, int64_t n_samples,
                              int32_t n_points)
 {
     const int64_t nb = (N / b_r) * (K / b_c), nv = n_samples + 2;
-    const int32_t chunk = rank_chunk(nb);
-    const int32_t n_chunks = (int32_t)((nb + chunk - 1) / chunk);
     // scores (nb), dots (nv x nb), step sums (points x nv), step terms
-    // (points), perm (nb), rank counts (n_chunks x nb)
+    // (points), perm (nb)
     return (size_t)(nb + nv * nb + (int64_t)n_points * nv + n_points) * sizeof(double) +
-           (size_t)(nb + (int64_t)n_chunks * nb) * sizeof(int32_t);
+           (size_t)nb * sizeof(int32_t);
 }
 
 hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
 {
     const int32_t R = (int32_t)(c.N / c.b_r), C = (int32_t)(c.K / c.b_c);
     const int64_t nb = (int64_t)R * C, nv = c.n_samples + 2;
-    const int32_t chunk = rank_chunk(nb);
-    const int32_t n_chunks = (int32_t)((nb + chunk - 1) / chunk);
     const size_t bytes = delta_workspace_bytes(c.N, c.K, c.b_r, c.b_c, c.n_samples, c.n_points);
     // the caller's workspace, else one allocated (and freed) on the stream
     char* ws = (char*)c.ws;
@@ -267,19 +269,12 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
     double* q = dots + nv * nb;
     double* term = q + (int64_t)c.n_points * nv;
     int32_t* perm = (int32_t*)(term + c.n_points);
-    int32_t* cnt = perm + nb;
     MaskCall m = {c.W, c.ldw, c.grad, c.ldg, c.N, c.K, c.dtype, c.b_r, c.b_c, 0, nullptr, scores};
     e = launch_block_scores(m, s);
     if (e == hipSuccess) {
-        const unsigned gx = (unsigned)((nb + 255) / 256);
-        hipLaunchKernelGGL(k_rank_counts, dim3(gx, (unsigned)n_chunks), dim3(256),
-                           (size_t)chunk * sizeof(uint64_t), s, (const double*)scores, nb, chunk, cnt);
+        hipLaunchKernelGGL(k_rank, dim3((unsigned)((nb + 63) / 64)), dim3(64 * RANK_WAVES), 0, s,
+                           (const double*)scores, nb, perm);
         e = hipGetLastError();
-        if (e == hipSuccess) {
-            hipLaunchKernelGGL(k_rank_scatter, dim3(gx), dim3(256), 0, s, (const int32_t*)cnt, nb,
-                               n_chunks, perm);
-            e = hipGetLastError();
-        }
     }
     if (e == hipSuccess) {
         const int64_t nch = c.K / 8;
@@ -310,7 +305,11 @@ hipError_t launch_delta_curve(const DeltaCall& c, hipStream_t s)
                            (const double*)dots, (const int32_t*)perm, q);
         e = hipGetLastError();
         if (e == hipSuccess) {
-            hipLaunchKernelGGL(k_delta_finish, dim3(1), dim3(1024), 0, s, c, q, term);
+            const size_t fin = (size_t)((int64_t)c.n_points * nv + c.n_points) * sizeof(double);
+            if (fin <= 65536)
+                hipLaunchKernelGGL(k_delta_finish<true>, dim3(1), dim3(1024), fin, s, c, q, term);
+            else
+                hipLaunchKernelGGL(k_delta_finish<false>, dim3(1), dim3(1024), 0, s, c, q, term);
             e = hipGetLastError();
         }
     }

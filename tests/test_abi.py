@@ -208,9 +208,9 @@ def test_delta_curve_workspace_size_and_checks(L):
                                                 ctypes.byref(sz) if out else None)
     assert ws() == OK
     # scores, dots of n + 2 vectors, per-point step sums and terms (float64),
-    # the permutation and the rank counts of 128-block chunks (int32)
+    # the permutation (int32)
     nb = 96 * 24
-    assert sz.value == (nb + 6 * nb + 21 * 6 + 21) * 8 + (nb + 18 * nb) * 4
+    assert sz.value == (nb + 6 * nb + 21 * 6 + 21) * 8 + nb * 4
     big = ws(N=768, K=3072, n=64, npt=128) == OK and sz.value
     assert big > (66 * 2304) * 8
     assert ws(b_r=8) == BLOCK and ws(N=3072 + 16) == SHAPE and ws(N=1 << 17) == SHAPE

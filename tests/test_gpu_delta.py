@@ -85,6 +85,13 @@ def test_delta_curve_widest_rows():
     check(W, grad, S, "bf16", 16, 16, 0.01, [0, 50, 100], "K = 65536")
 
 
+def test_delta_curve_many_blocks():
+    # 32768 blocks of 16 x 16: the ranking kernel's key range split over its
+    # 16 waves, 512 workgroups
+    W, grad, S = inputs(107, 2048, 4096, 1, "bf16")
+    check(W, grad, S, "bf16", 16, 16, 0.01, [0, 33, 67, 100], "32768 blocks")
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_delta_curve_caller_workspace(dtype):
     # lpv_delta_curve_ws with a caller-owned workspace gives the curve of
@@ -108,3 +115,32 @@ def test_delta_curve_caller_workspace(dtype):
         assert np.abs(b.cpu().numpy() - ref).max() <= TOL * max(np.abs(ref).max(), 1e-300)
     with pytest.raises(lpv.LpvError):
         lpv.delta_curve(Wd, Gd, Sd, 16, 32, 0.1, pcts, workspace=ws[:64])
+
+
+def test_delta_curve_many_points_and_samples():
+    # 128 points x 72 vectors of step sums (74 KB): more than the finishing
+    # kernel stages in LDS, so it runs on global memory
+    W, grad, S = inputs(110, 64, 128, 70, "bf16")
+    pcts = sorted(np.random.default_rng(111).integers(0, 101, 128).tolist())
+    check(W, grad, S, "bf16", 16, 16, 0.02, pcts, "128 points")
+
+
+def test_delta_curve_queued_calls_on_a_side_stream():
+    # three calls queued back to back on a non-default stream (no
+    # synchronisation in between, each with its own stream-ordered
+    # workspace), each against the oracle
+    pcts = [0, 20, 40, 60, 80, 100]
+    cases = [inputs(112 + i, 128, 192, 3 + i, "bf16") for i in range(3)]
+    st = torch.cuda.Stream()
+    outs = []
+    with torch.cuda.stream(st):
+        for (W, grad, S), (b_r, b_c) in zip(cases, ((32, 32), (16, 16), (32, 64))):
+            Sd = dev(S.reshape(S.shape[0], -1), "bf16").reshape(S.shape)
+            outs.append(lpv.delta_curve(dev(W, "bf16"), dev(grad, "bf16"), Sd, b_r, b_c, 0.1, pcts,
+                                        stream=st))
+    st.synchronize()
+    for (W, grad, S), (b_r, b_c), got in zip(cases, ((32, 32), (16, 16), (32, 64)), outs):
+        ref = oracle.delta_curve(W, "bf16", b_r, b_c, grad, S, 0.1, pcts)
+        err = np.abs(got.cpu().numpy() - ref).max() / max(np.abs(ref).max(), 1e-300)
+        say("delta_curve queued", (b_r, b_c), "rel err %.2e" % err)
+        assert err <= TOL
