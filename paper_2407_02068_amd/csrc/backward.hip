@@ -246,6 +246,17 @@ __device__ inline void gw_dma(const void* src, uint32_t m0)
         : "memory");
 }
 
+// The same from a wave-uniform base (saddr) and a per-lane 32-bit offset.
+__device__ inline void gw_dma_off(const char* base, uint32_t off, uint32_t m0)
+{
+    asm volatile(
+        "s_nop 0\n"
+        "global_load_lds_dwordx4 %0, %1"
+        :
+        : "v"(off), "s"(base), "{m0}"(m0)
+        : "memory");
+}
+
 typedef short v4s __attribute__((ext_vector_type(4)));
 
 __device__ inline v4s tr_read(uint32_t addr)
@@ -270,15 +281,17 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    // Items (chunk, window), chunk-major with groups fastest, are dealt to
-    // XCDs in contiguous runs (workgroup b runs on XCD b % 8): the items that
-    // share a chunk's rows of G and X then mostly share one L2.
+    // Items (chunk, window), chunk-major with window columns fastest, are
+    // dealt to XCDs in contiguous runs (workgroup b runs on XCD b % 8): the
+    // items that share a chunk's rows of G and X then mostly share one L2, and
+    // a chunk whose items fall on two XCDs splits between groups, so that
+    // each group's slice of G is still read by about one XCD.
     const int n_win = d.n_groups * d.n_wcols;
     const int item = (int)(blockIdx.x & 7) * d.per_xcd + (int)(blockIdx.x >> 3);
     if (item >= n_win * d.n_chunks)
         return;
     const int chunk = item / n_win, win = item - chunk * n_win;
-    const int g = win % d.n_groups, wc = win / d.n_groups;
+    const int g = win / d.n_wcols, wc = win - g * d.n_wcols;
     const int64_t m_begin = (int64_t)chunk * d.chunk_rows;
     const int64_t m_end = min(d.M, m_begin + d.chunk_rows);
 
@@ -343,12 +356,14 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
         }
     }
 
-    // DMA: wave w fills rows 4w .. 4w + 3 of the G and the X part of a stage
-    // (two 1 KB instructions each); LDS chunk q (16 bytes) of row r holds
-    // columns 32 (seg ^ swz(r)) + 8 (q % 4) .. + 7 with seg = q / 4.
+    // DMA: wave w fills rows 8w .. 8w + 7 of the G and the X part of a stage
+    // (four 1 KB instructions each, two rows apiece); LDS chunk q (16 bytes)
+    // of row r holds columns 32 (seg ^ swz(r)) + 8 (q % 4) .. + 7 with
+    // seg = q / 4.
     const uint32_t smem0 = lds_u32(smem);
     int drow[GW_DMA];
     int64_t gcol[GW_DMA], xcol[GW_DMA];
+    uint32_t gvo[GW_DMA], xvo[GW_DMA];  // byte offsets within a token step's rows
 #pragma unroll
     for (int i = 0; i < GW_DMA; ++i) {
         drow[i] = (GW_TOK / 8) * wave + 2 * i + (lane >> 5);
@@ -356,12 +371,31 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
         const int col = 32 * ((q >> 2) ^ gw_swz(drow[i])) + 8 * (q & 3);
         gcol[i] = min((int64_t)g * 256 + col, d.N - 8);  // past the edge: any valid
         xcol[i] = min((int64_t)wc * 256 + col, d.K - 8);  // columns (never kept)
+        // (fit 32 bits: 64 rows of a leading dimension of at most 2^22)
+        gvo[i] = (uint32_t)((drow[i] * d.ldg + gcol[i]) * 2);
+        xvo[i] = (uint32_t)((drow[i] * d.ldx + xcol[i]) * 2);
     }
     const int64_t n_steps = (m_end - m_begin + GW_TOK - 1) / GW_TOK;
-    // issue the DMA of token step st into its stage
+    const char* g0 = G + m_begin * d.ldg * 2;
+    const char* x0 = X + m_begin * d.ldx * 2;
+    const int64_t g_step = (int64_t)GW_TOK * d.ldg * 2, x_step = (int64_t)GW_TOK * d.ldx * 2;
+    // issue the DMA of token step st into its stage: a step whose rows all
+    // lie in the chunk from a wave-uniform row base and the fixed per-lane
+    // offsets; the chunk's last, partial step row by row (rows past the chunk
+    // read the zero line for G, and X rows past M repeat the last)
     auto dma_step = [&](int64_t st) {
         const uint32_t base = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE +
                               (uint32_t)wave * (GW_TOK / 8) * 512;
+        if (m_begin + (st + 1) * GW_TOK <= m_end) {
+            const char* gb = g0 + st * g_step;
+            const char* xb = x0 + st * x_step;
+#pragma unroll
+            for (int i = 0; i < GW_DMA; ++i) {
+                gw_dma_off(gb, gvo[i], base + i * 1024);
+                gw_dma_off(xb, xvo[i], base + GW_XOFF + i * 1024);
+            }
+            return;
+        }
 #pragma unroll
         for (int i = 0; i < GW_DMA; ++i) {
             const int64_t m = m_begin + st * GW_TOK + drow[i];
@@ -372,32 +406,22 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
         }
     };
 
-    // transposed operand reads: (k-step ks, half h) -> row and byte offset
-    // within the row; the segment is the tile row (G) or tile column (X)
-    uint32_t roff[GW_KS][2], rswz[GW_KS][2];
-    {
-        const int q16 = lane >> 4, j16 = lane & 15;
-#pragma unroll
-        for (int ks = 0; ks < GW_KS; ++ks)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int row = ks * 16 + 8 * (q16 >> 1) + 4 * h + (j16 >> 2);
-                roff[ks][h] = (uint32_t)(row * 512 + 32 * (q16 & 1) + 8 * (j16 & 3));
-                rswz[ks][h] = (uint32_t)(gw_swz(row) << 6);
-            }
-    }
-    auto frag = [&](uint32_t stage, int ks, int seg) {
-        const uint32_t s6 = (uint32_t)seg << 6;
-        const v4s lo4 = tr_read(stage + roff[ks][0] + (s6 ^ rswz[ks][0]));
-        const v4s hi4 = tr_read(stage + roff[ks][1] + (s6 ^ rswz[ks][1]));
+    // Transposed operand reads.  Fragment (k-step ks, half h) of lane (q16 =
+    // lane / 16, j16 = lane % 16) is row 16 ks + 8 (q16 / 2) + 4 h + j16 / 4,
+    // byte 32 (q16 % 2) + 8 (j16 % 4) of its 64-byte segment; the segment (the
+    // tile row for G, the tile column for X) sits at (seg ^ swz(row)) 64, and
+    // swz(row) = j16 / 4 + 4 (q16 / 2) is the same for all of the lane's rows.
+    // So each fragment is a per-lane base (per kept tile, fixed for the whole
+    // chunk) plus the stage and the constant 8192 ks + 2048 h.
+    const int q16 = lane >> 4, j16 = lane & 15;
+    const uint32_t sw = (uint32_t)((j16 >> 2) | ((q16 >> 1) << 2));
+    const uint32_t r0 = (uint32_t)((8 * (q16 >> 1) + (j16 >> 2)) * 512 + 32 * (q16 & 1) + 8 * (j16 & 3));
+    auto frag = [&](uint32_t addr, int ks) {
+        const v4s lo4 = tr_read(addr + ks * 8192);
+        const v4s hi4 = tr_read(addr + ks * 8192 + 2048);
         const v4s both[2] = {lo4, hi4};
         return __builtin_bit_cast(F, both);
     };
-
-    f32x16 acc[8];
-#pragma unroll
-    for (int t = 0; t < 8; ++t)
-        acc[t] = f32x16{};
 
     // prologue: step 0
     dma_step(0);
@@ -405,6 +429,16 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
     // constant (one copy of the loop per count): no per-tile test in the loop
     auto steps = [&](auto nw_c) {
         constexpr int NW = decltype(nw_c)::value;
+        constexpr int NA = NW > 0 ? NW : 1;
+        const uint32_t ga = r0 + (((uint32_t)tj ^ sw) << 6);
+        uint32_t xa[NA];
+#pragma unroll
+        for (int t = 0; t < NA; ++t)
+            xa[t] = r0 + GW_XOFF + (((uint32_t)tc[t] ^ sw) << 6);
+        f32x16 acc[NA];
+#pragma unroll
+        for (int t = 0; t < NA; ++t)
+            acc[t] = f32x16{};
         for (int64_t st = 0; st < n_steps; ++st) {
             // step st's DMA (the wave's only one in flight) has landed; the
             // barrier publishes it to everyone and frees the stage of step
@@ -413,18 +447,38 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
             if (st + 1 < n_steps)
                 dma_step(st + 1);
             const uint32_t stage = smem0 + (uint32_t)(st % GW_NSTG) * GW_STAGE;
+            // one G fragment for the row and one X fragment per kept tile;
+            // those of k-step ks + 1 are read before k-step ks's products
+            F a[2], b[2][NA];
+            a[0] = frag(stage + ga, 0);
+#pragma unroll
+            for (int t = 0; t < NW; ++t)
+                b[0][t] = frag(stage + xa[t], 0);
 #pragma unroll
             for (int ks = 0; ks < GW_KS; ++ks) {
-                // one G fragment for the row, one X fragment per kept tile,
-                // each in registers of its own; then the products
-                const F a = frag(stage, ks, tj);
-                F b[NW > 0 ? NW : 1];
+                if (ks + 1 < GW_KS) {
+                    a[(ks + 1) & 1] = frag(stage + ga, ks + 1);
+#pragma unroll
+                    for (int t = 0; t < NW; ++t)
+                        b[(ks + 1) & 1][t] = frag(stage + xa[t], ks + 1);
+                }
+                // (the scheduler keeps the reads above ahead of the products)
+                __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
                 for (int t = 0; t < NW; ++t)
-                    b[t] = frag(stage + GW_XOFF, ks, tc[t]);
+                    acc[t] = E::mma(a[ks & 1], b[ks & 1][t], acc[t]);
+            }
+        }
+        // partials of this chunk
 #pragma unroll
-                for (int t = 0; t < NW; ++t)
-                    acc[t] = E::mma(a, b[t], acc[t]);
+        for (int t = 0; t < NW; ++t) {
+            const int64_t tile = (int64_t)(8 * g + tj) * d.n_tile_cols + (8 * wc + tc[t]);
+            float* dst = ws + ((int64_t)chunk * d.n_tile_rows * d.n_tile_cols + tile) * 1024;
+#pragma unroll
+            for (int qq = 0; qq < 4; ++qq) {
+                const float4 v = {acc[t][4 * qq], acc[t][4 * qq + 1], acc[t][4 * qq + 2],
+                                  acc[t][4 * qq + 3]};
+                *(float4*)(dst + qq * 256 + lane * 4) = v;
             }
         }
     };
@@ -438,21 +492,6 @@ __global__ __launch_bounds__(GW_NT, 1) void k_gradw_tiles(const GradWDims d,
     case 6: steps(std::integral_constant<int, 6>{}); break;
     case 7: steps(std::integral_constant<int, 7>{}); break;
     default: steps(std::integral_constant<int, 8>{}); break;
-    }
-
-    // partials of this chunk
-#pragma unroll
-    for (int t = 0; t < 8; ++t) {
-        if (t < n_w) {
-            const int64_t tile = (int64_t)(8 * g + tj) * d.n_tile_cols + (8 * wc + tc[t]);
-            float* dst = ws + ((int64_t)chunk * d.n_tile_rows * d.n_tile_cols + tile) * 1024;
-#pragma unroll
-            for (int qq = 0; qq < 4; ++qq) {
-                const float4 v = {acc[t][4 * qq], acc[t][4 * qq + 1], acc[t][4 * qq + 2],
-                                  acc[t][4 * qq + 3]};
-                *(float4*)(dst + qq * 256 + lane * 4) = v;
-            }
-        }
     }
 }
 
