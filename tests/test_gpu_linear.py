@@ -334,25 +334,33 @@ def _table_bytes(w):
     """Per-launch table bytes of the block-sparse kernel if every group of 8
     tile rows (256 outputs) went into one launch: 16 B per slot descriptor,
     1 KB of float32 bias per group, 16 B per walk entry (the tile columns the
-    group keeps a tile in, padded to an even count).  32 x 32 blocks only."""
-    assert w.b_r == 32 and w.b_c == 32
+    group keeps a tile in, padded to an even count).  Square blocks of 16 or
+    32 (a 32 x 32 tile is kept when any block it covers is)."""
+    assert w.b_r == w.b_c and w.b_r in (16, 32)
+    m = w.mask
+    if w.b_r == 16:
+        R, C = m.shape
+        m = m.reshape(R // 2, 2, C // 2, 2).any(axis=(1, 3))
     total = 0
-    for g0 in range(0, w.mask.shape[0], 8):
-        steps = int(w.mask[g0:g0 + 8].any(axis=0).sum())
+    for g0 in range(0, m.shape[0], 8):
+        steps = int(m[g0:g0 + 8].any(axis=0).sum())
         total += 16 + 1024 + 16 * (steps + (steps & 1))
     return total
 
 
-@pytest.mark.parametrize("N,K", [(8192, 768), (4096, 3072)])
-def test_multi_launch_tables(N, K):
+@pytest.mark.parametrize("N,K,block", [(8192, 768, 32), (4096, 3072, 32), (8192, 768, 16)])
+def test_multi_launch_tables(N, K, block):
     """Layers wide enough that the kernel's per-launch tables (walk, slot
     descriptors, bias) exceed the 32 KB it keeps in LDS: the call is split into
-    several launches over runs of output groups.  Sparse with GELU, and dense."""
-    w = wl.custom(75, 300, N, K, 32, 32, "bf16", "uniform", 50, gelu=True)
+    several launches over runs of output groups.  Sparse with GELU (also with
+    16 x 16 blocks, whose walk entries carry per-half row bits), and dense."""
+    w = wl.custom(75, 300, N, K, block, block, "bf16", "uniform", 50, gelu=True)
     assert _table_bytes(w) > 32 * 1024
-    say("multi-launch", N, K, "nnzb", w.nnzb)
+    say("multi-launch", N, K, block, "nnzb", w.nnzb)
     _, Y = run_bsr(w)
     assert_close(f64(Y), ref(w), "bf16", w.name)
+    if block == 16:
+        return
     Yd = lpv.dense_linear(dev(w.W, "bf16"), dev(w.X, "bf16"), dev(w.bias, "bf16"), epi="gelu")
     torch.cuda.synchronize()
     r = oracle.linear(w.X, w.W, "bf16", 32, 32, np.ones_like(w.mask), w.bias, gelu=True)
