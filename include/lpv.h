@@ -160,7 +160,8 @@ lpv_status lpv_bsr_unpack(const lpv_bsr* h, void* W_out, int64_t ldw, void* stre
  *       256-token slice of X with 32-bit byte offsets).
  * bias  device, N elements, or NULL for no bias.
  * Y     device, M x N, row stride ldy >= N; must not overlap X.
- * epi   LPV_EPI_NONE or LPV_EPI_GELU (exact-erf GELU after the bias).
+ * epi   LPV_EPI_NONE or LPV_EPI_GELU (x Phi(x) with the error function, after
+ *       the bias, in float32 to 5e-6 relative).
  *
  * The product of the input with the block-sparse weight of Sec. 3.4: each
  * token tile times each group of output tile rows walks only the kept tiles
