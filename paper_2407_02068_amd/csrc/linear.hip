@@ -23,7 +23,8 @@
 //     the pair's kept W tiles (tile j by wave j, two instructions per step),
 //     one pair ahead, 16 bytes per lane with no registers in between;
 //   - each step's row bits travel from the producer cursor to the consumer in
-//     a 64-bit queue (12 bits per step in flight); the wait before each pair's
+//     a 64-bit queue (12 bits per step in flight; KH: the rows keeping the
+//     second 16 columns in a second, 32-bit queue); the wait before each pair's
 //     barrier (vmcnt(0)) covers the next pair's DMA and a finished item's
 //     stores, and the barrier tells every wave that the pair landed and that
 //     the pair slot read before it is free;
@@ -37,9 +38,11 @@
 // the per-group descriptors (group, first step, step count, first column
 // walked) are built at pack time, item coordinates advance by constants, and
 // the walk is read one 64-entry segment ahead.
-// The epilogue adds the bias, applies GELU if asked, rounds once to the element
-// type and stores Y (16 bytes per lane, transposed through LDS), while the DMA
-// of the next item's first pair is already in flight.
+// The epilogue adds the bias (the accumulators start at it), applies GELU if
+// asked, rounds once to the element type and stores Y (16 bytes per lane,
+// transposed through LDS).  The next item's first pair, whose DMA went out
+// during this item's last pair, has landed by then; the stores leave after the
+// next barrier, beside the DMA of the pair after it.
 //
 // MFMA operand roles: A = a W tile (rows = output features), B = X slice
 // transposed (columns = tokens), so D[n][token]: lane l holds token l % 32 and,
