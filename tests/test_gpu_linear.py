@@ -149,11 +149,13 @@ def test_deterministic_and_token_permutation():
     assert torch.equal(Yp.view(torch.int16), Y1[perm].view(torch.int16))
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_strided_views_and_guard_bands(dtype):
+@pytest.mark.parametrize("dtype,b_c,K", [("bf16", 32, 192), ("bf16", 16, 176), ("f32", 16, 192)])
+def test_strided_views_and_guard_bands(dtype, b_c, K):
     """X read through a column slice of a wider buffer (ldx > K); Y written
-    into the middle of a padded buffer (ldy > N) whose canaries must survive."""
-    w = wl.custom(65, 197, 256, 192, 32, 16 if dtype == "f32" else 32, dtype, "uniform", 40)
+    into the middle of a padded buffer (ldy > N) whose canaries must survive.
+    Also with 16-wide block columns and a 16-column reduction tail (the
+    half-tile walk and the zero line in place of X past K)."""
+    w = wl.custom(65, 197, 256, K, 32, b_c, dtype, "uniform", 40)
     tt = TORCH[dtype]
     big = torch.zeros((w.M, 3 * w.K), dtype=tt, device="cuda")
     big[:, w.K:2 * w.K] = dev(w.X, dtype)
