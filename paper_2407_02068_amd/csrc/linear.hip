@@ -23,9 +23,9 @@
 //     the pair's kept W tiles (tile j by wave j, two instructions per step),
 //     one pair ahead, 16 bytes per lane with no registers in between;
 //   - each step's row bits travel from the producer cursor to the consumer in
-//     a 64-bit queue (12 bits per step in flight; KH: the rows keeping the
-//     second 16 columns in a second, 32-bit queue); the wait before each pair's
-//     barrier (vmcnt(0)) covers the next pair's DMA and a finished item's
+//     a 64-bit queue (12 bits per step in flight: the wave's own four rows,
+//     per 16-column half with KH, and the item's end); the wait before each
+//     pair's barrier (vmcnt(0)) covers the next pair's DMA and a finished item's
 //     stores, and the barrier tells every wave that the pair landed and that
 //     the pair slot read before it is free;
 //   - wave (m, h) takes tokens [64m, 64m + 64) and tile rows [4h, 4h + 4) of
@@ -139,13 +139,6 @@ template <int IMM> __device__ inline void dma16i(const char* saddr, uint32_t vof
         : "memory");
 }
 
-// s_waitcnt vmcnt(n) (gfx9 encoding; expcnt and lgkmcnt left alone)
-template <int N> __device__ inline void wait_vm()
-{
-    static_assert(N < 64, "vmcnt is 6 bits");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
 typedef int v4i __attribute__((ext_vector_type(4)));
 
 // 16-byte LDS read at a byte address (an ordinary load: the compiler places
@@ -177,10 +170,11 @@ __device__ inline int xswz(int r) { return (r >> 1) & 7; }
 // memory access.
 constexpr int W_LAST = 1 << 24, W_SEG_END = 1 << 25;
 constexpr int SEG = 64;
-// Queue entry of one step in flight (12 bits, up to 5 in a 64-bit queue): row
-// bits (8), last step of its item (bit 8), a real step (bit 9; entries past
-// the last item are 0).
-constexpr int E_LAST = 1 << 8, E_VALID = 1 << 9, E_BITS = 12, E_MASK = (1 << E_BITS) - 1;
+// Queue entry of one step in flight (12 bits, up to 5 in a 64-bit queue): the
+// kept rows among the wave's four (bit j: row 4 h + j of the group) for the
+// first k-step (bits 0..3) and, with 16-wide block columns, the second (bits
+// 4..7; otherwise the first serves both), and the item's last step (bit 8).
+constexpr int E_LAST = 1 << 8, E_BITS = 12, E_MASK = (1 << E_BITS) - 1;
 
 template <int DT, bool GELU, bool DENSE, bool KTAIL, bool KH>
 __global__ __launch_bounds__(NT, 1) void k_linear16(
@@ -196,6 +190,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform per wave
     const int wm = wave & 3, wh = wave >> 2;
+    const int wsh = 4 * wh;  // this wave's rows in a group's row bits
 
     // This workgroup's items.  Items are (token tile, launch slot) pairs,
     // slot-minor; workgroup b runs on XCD x = b % 8 as its c = b / 8-th of
@@ -378,33 +373,24 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // tile), the column tile and its byte offset in a row of X / dense W, and
     // (sparse) the byte offset of this wave's W tile in the tile stream.
     // KH: the halves of this wave's tile to load (hl: bit 0 the first 16
-    // columns, bit 1 the second) and the step's rows that keep the second
-    // half (hq, for the consumer).
+    // columns, bit 1 the second).
     struct Dma {
-        int slot, n, col, hl, hq;
+        int slot, n, col, hl;
         uint32_t xcol, woff;
     };
-    bool x_stale = false;  // the item advanced: set_x() before the next step
-    int p_rows = n_full == 0 ? 0xf << (4 * hh) : 0xff;  // rows the producer's item keeps
+    bool x_stale = false;  // the item advanced: set_x() before the next pair
+    // rows the producer's item keeps (none past the last item: the producer
+    // then keeps walking, inside the table, and its steps load nothing)
+    int p_rows = n_full == 0 ? 0xf << (4 * hh) : 0xff;
     auto p_prepare = [&](int slot, Dma& d) -> int {
-        // (the previous step's DMA, issued after its p_prepare, used the old
-        // item's bases)
-        if (x_stale) {
-            set_x();
-            x_stale = false;
-        }
         d.slot = slot;
         d.n = 0;
-        d.col = 0;
         d.hl = 0;
-        d.hq = 0;
-        d.xcol = 0;
         d.woff = 0;
-        if (pk >= my_items)
-            return 0;
         const int ex = __builtin_amdgcn_readlane(cur.x, p_i);
-        const int col = ex & 0xffff;
-        int lo_bits = (ex >> 16) & 0xff, hi_bits = lo_bits, all_bits = lo_bits;
+        // row bits in 0..7, the item's last step in bit 8 (= E_LAST)
+        const int es = (int)((uint32_t)ex >> 16);
+        int lo_bits = es & 0xff, hi_bits = lo_bits, all_bits = lo_bits;
         int tile0 = 0;
         if (KH) {
             const int ey = __builtin_amdgcn_readlane(cur.y, p_i);
@@ -415,9 +401,10 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         // a half item keeps its own half's rows (the tile stream order, and so
         // a tile's rank, still counts every kept row of the step)
         const int bits = all_bits & p_rows;
-        d.col = col;
-        d.xcol = (uint32_t)col * (TILE * 2);
-        d.n = bits ? 2 : 0;  // a step that keeps no tile (walk padding) loads nothing
+        d.col = ex & 0xffff;
+        d.xcol = (uint32_t)d.col * (TILE * 2);
+        if (bits)  // a step that keeps no tile (walk padding) loads nothing
+            d.n = 2;
         if (DENSE) {
             if (bits)
                 d.n = 4;
@@ -429,38 +416,54 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             if (KH)
                 d.hl = ((lo_bits >> wave) & 1) | (((hi_bits >> wave) & 1) << 1);
         }
-        if (KH)
-            d.hq = hi_bits & p_rows;
-        const int e = (KH ? lo_bits & p_rows : bits) | ((ex & W_LAST) ? E_LAST : 0) | E_VALID;
+        // the queue entry (p_rows clears the other half's rows in a half item,
+        // and every row past the last item)
+        const int e_lo = ((KH ? lo_bits & p_rows : bits) >> wsh) & 15;
+        const int e_hi = KH ? (((hi_bits & p_rows) >> wsh) & 15) << 4 : 0;
+        const int e = e_lo | e_hi | (es & E_LAST);
         // advance: next entry of the segment, or the next segment (whose
         // successor is read now; every half step waits for LDS reads)
-        if (ex & W_SEG_END) {
+        if (__builtin_expect(ex & W_SEG_END, 0)) {
             cur = nxt;
             p_i = 0;
             nxt = seg_read(__builtin_amdgcn_readlane(cur.z, 0));
         } else {
             ++p_i;
         }
-        if ((ex & W_LAST) && ++pk < my_items) {
-            if (pk == n_full) {
-                // on to the half item: its walk replaces the prefetched one
-                p_rows = 0xf << (4 * hh);
-                p_slot = h_slot;
-                p_mt = h_mt;
-                cur = seg_read(t_desc[h_slot].y);
-                nxt = seg_read(__builtin_amdgcn_readlane(cur.z, 0));
-                p_i = 0;
-            } else {
-                p_slot += a.p_mod;
-                p_mt += a.p_div;
-                if (p_slot >= a.n_slots) {
-                    p_slot -= a.n_slots;
-                    p_mt += a.mt_carry;
+        if (__builtin_expect(ex & W_LAST, 0)) {
+            if (++pk < my_items) {
+                if (pk == n_full) {
+                    // on to the half item: its walk replaces the prefetched one
+                    p_rows = 0xf << (4 * hh);
+                    p_slot = h_slot;
+                    p_mt = h_mt;
+                    cur = seg_read(t_desc[h_slot].y);
+                    nxt = seg_read(__builtin_amdgcn_readlane(cur.z, 0));
+                    p_i = 0;
+                } else {
+                    p_slot += a.p_mod;
+                    p_mt += a.p_div;
+                    if (p_slot >= a.n_slots) {
+                        p_slot -= a.n_slots;
+                        p_mt += a.mt_carry;
+                    }
                 }
+                // (items have an even number of steps: the next pair is the
+                // new item's first)
+                x_stale = true;
+            } else {
+                p_rows = 0;
             }
-            x_stale = true;
         }
         return e;
+    };
+    auto x_fresh = [&]() {
+        // (the previous pair's DMA, issued after its p_prepare, used the old
+        // item's bases)
+        if (x_stale) {
+            set_x();
+            x_stale = false;
+        }
     };
     // The DMA of a pair of prepared steps (d0, d1) into their pair slot, in
     // two parts.  X: 4 instructions of one M0 value (none if neither step
@@ -544,13 +547,10 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
 
     // ---- prologue: the first pair of steps
     uint64_t q = 0;  // queue entries of steps t, t + 1, ... (E_BITS each)
-    uint32_t qh = 0;  // KH: their second-half row bits, 8 each
     {
         Dma d0, d1;
         q |= (uint64_t)(uint32_t)p_prepare(0, d0);
         q |= (uint64_t)(uint32_t)p_prepare(1, d1) << E_BITS;
-        if (KH)
-            qh |= (uint32_t)d0.hq | (uint32_t)d1.hq << 8;
         dma_x(d0, d1);
         dma_w(d0, d1);
     }
@@ -633,7 +633,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // first half of step t: the second half's operands are read, then (t,
     // k-step 0) goes to the matrix cores
     auto half_a = [&](int t, int bits) {
-        int bh = (bits >> (4 * wh)) & 15;
+        int bh = bits;
         // opaque to the compiler: a kept-row test is then one scalar bit test
         // and branch, not a 64-bit mask kept for the other half step
         asm volatile("" : "+s"(bh));
@@ -650,7 +650,7 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
     // second half of step t: (t, k-step 1), while the first half of step t + 1
     // is read if it belongs to the same pair
     auto half_b = [&](int t, int bits, bool pre) {
-        int bh = (bits >> (4 * wh)) & 15;
+        int bh = bits;
         asm volatile("" : "+s"(bh));
         if (pre)
             read_half(r0, t + 1, 0);
@@ -785,10 +785,9 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         read_half(r0, t, 0);
         {
             Dma d0, d1;
+            x_fresh();
             q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
             q |= (uint64_t)(uint32_t)p_prepare((t + 3) & (NS - 1), d1) << (3 * E_BITS);
-            if (KH)
-                qh |= (uint32_t)d0.hq << 16 | (uint32_t)d1.hq << 24;
             dma_x(d0, d1);
             if (have)
                 flush(((t + 2) >> 1) & 1);
@@ -798,24 +797,22 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
         for (;;) {  // the pairs of the item
             const int e0 = (int)(q & E_MASK), e1 = (int)((q >> E_BITS) & E_MASK);
             // rows of each step that keep the second k-step (KH: their own bits)
-            const int h0 = KH ? (int)(qh & 0xff) : e0 & 0xff;
-            const int h1 = KH ? (int)((qh >> 8) & 0xff) : e1 & 0xff;
-            half_a(t, e0 & 0xff);
+            const int h0 = KH ? (e0 >> 4) & 15 : e0 & 15;
+            const int h1 = KH ? (e1 >> 4) & 15 : e1 & 15;
+            half_a(t, e0 & 15);
             half_b(t, h0, true);
-            half_a(t + 1, e1 & 0xff);
+            half_a(t + 1, e1 & 15);
             half_b(t + 1, h1, false);
             q >>= 2 * E_BITS;
-            qh >>= 16;
             t += 2;
             sync();
             if (e1 & E_LAST)
                 break;
             read_half(r0, t, 0);
             Dma d0, d1;
+            x_fresh();
             q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
             q |= (uint64_t)(uint32_t)p_prepare((t + 3) & (NS - 1), d1) << (3 * E_BITS);
-            if (KH)
-                qh |= (uint32_t)d0.hq << 16 | (uint32_t)d1.hq << 24;
             dma_x(d0, d1);
             dma_w(d0, d1);
         }
