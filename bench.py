@@ -66,8 +66,10 @@ def algorithmic_bytes(M, N, K, nnzb, b_r, b_c, kused_cols, es=2):
     return es * (M * kused_cols + M * N + nnzb * b_r * b_c + N) + 4 * (N // b_r + 1 + nnzb)
 
 
-SPARSE_KERNEL = "k_linear16<2, false, false, false, false>"  # bf16, no GELU, block-sparse, 32-wide blocks
-DENSE_KERNEL = "k_linear16<2, false, true, false, false>"    # bf16, no GELU, dense
+# bf16, no GELU, block-sparse with 32-wide blocks / dense; 12 groups of 256
+# outputs, so the pair's last k-step is multiplied after its barrier
+SPARSE_KERNEL = "k_linear16<2, false, false, false, false, true>"
+DENSE_KERNEL = "k_linear16<2, false, true, false, false, true>"
 CALIB_BYTES = 1 << 30                        # the calibration copy reads and writes this much
 
 
@@ -114,13 +116,15 @@ def write_traffic(fetch_csv, write_csv, command):
 def kernel_label(name):
     """A short name for a kernel of the rocprofv3 statistics."""
     import re
-    m = re.search(r"k_linear16<(\d), (true|false), (true|false), (true|false), (true|false)>", name)
+    m = re.search(r"k_linear16<(\d), (true|false), (true|false), (true|false), (true|false), (true|false)>",
+                  name)
     if m:
-        return "k_linear16 %s %s%s%s%s (%s)" % (
+        return "k_linear16 %s %s%s%s%s%s (%s)" % (
             {"2": "bf16", "1": "fp16"}[m.group(1)],
             "dense" if m.group(3) == "true" else "block-sparse",
             " + GELU" if m.group(2) == "true" else "", ", K tail" if m.group(4) == "true" else "",
             ", 16-column halves" if m.group(5) == "true" else "",
+            ", DMA before the last k-step" if m.group(6) == "false" else "",
             "lpv_dense_linear" if m.group(3) == "true" else "lpv_bsr_linear")
     labels = (("k_block_scores_lds<2, true", "k_block_scores_lds, Taylor (lpv_delta_curve)"),
               ("k_block_scores_lds<2, false", "k_block_scores_lds, sum of squares (lpv_mask_topk)"),

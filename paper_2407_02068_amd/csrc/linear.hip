@@ -33,7 +33,8 @@
 //     accumulate) for each kept tile; the two waves of a SIMD cover both row
 //     halves, so every SIMD gets the step's whole kept count.  Each half step
 //     reads the next half step's fragments while its own go to the matrix
-//     cores.
+//     cores; with many groups per token tile (LATE) a pair's last k-step is
+//     multiplied after the barrier, over the next pair's first reads.
 // The step loop carries no division and no scalar load on its critical path:
 // the per-group descriptors (group, first step, step count, first column
 // walked) are built at pack time, item coordinates advance by constants, and
@@ -176,7 +177,7 @@ constexpr int SEG = 64;
 // 4..7; otherwise the first serves both), and the item's last step (bit 8).
 constexpr int E_LAST = 1 << 8, E_BITS = 12, E_MASK = (1 << E_BITS) - 1;
 
-template <int DT, bool GELU, bool DENSE, bool KTAIL, bool KH>
+template <int DT, bool GELU, bool DENSE, bool KTAIL, bool KH, bool LATE>
 __global__ __launch_bounds__(NT, 1) void k_linear16(
     const Dims a, const char* __restrict__ X, const char* __restrict__ stream,
     const int4* __restrict__ gdesc, const int2* __restrict__ walk,
@@ -802,13 +803,26 @@ __global__ __launch_bounds__(NT, 1) void k_linear16(
             half_a(t, e0 & 15);
             half_b(t, h0, true);
             half_a(t + 1, e1 & 15);
-            half_b(t + 1, h1, false);
             q >>= 2 * E_BITS;
             t += 2;
-            sync();
-            if (e1 & E_LAST)
-                break;
-            read_half(r0, t, 0);
+            if (LATE) {
+                // the last k-step's operands are in registers before the
+                // barrier lets the pair slot be refilled; its products keep
+                // the matrix cores busy while the next fragments are read and
+                // the next DMA is prepared
+                __builtin_amdgcn_s_waitcnt(0xc07f);
+                sync();
+                read_half(r0, t, 0);
+                half_b(t - 1, h1, false);
+                if (e1 & E_LAST)
+                    break;
+            } else {
+                half_b(t - 1, h1, false);
+                sync();
+                if (e1 & E_LAST)
+                    break;
+                read_half(r0, t, 0);
+            }
             Dma d0, d1;
             x_fresh();
             q |= (uint64_t)(uint32_t)p_prepare((t + 2) & (NS - 1), d0) << (2 * E_BITS);
@@ -955,6 +969,11 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
         const int64_t plain_max = (items + P - 1) / P;
         const int64_t xcd_max = ((n_mt + 7) / 8 * ns + C - 1) / C;
         d.xcd_tiles = n_mt >= 8 && xcd_max <= plain_max;
+        // Multiplying a pair's last k-step after its barrier fills the time
+        // the next fragments take to arrive but issues the next DMA later:
+        // it pays when a token tile's X is shared through L2 by many groups
+        // and costs when the DMA lead is the bound (few groups, long K).
+        const bool late = a.d.n_groups >= 6;
         if (d.xcd_tiles) {
             d.p_div = 8 * (C / ns);
             d.p_mod = C % ns;
@@ -965,9 +984,17 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
             d.mt_carry = 1;
         }
         const dim3 grid(P), block(NT);
+#define LPV_LAUNCH2(DT_, GELU_, KT_, KH_, LATE_)                                                   \
+    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_, KH_, LATE_>), grid, block, 0, s, d,    \
+                       a.X, a.stream, a.gdesc, a.walk, a.W, a.bias, a.Y)
+        // (the rare reduction-tail kernels come in one order only)
 #define LPV_LAUNCH1(DT_, GELU_, KT_, KH_)                                                         \
-    hipLaunchKernelGGL((k_linear16<DT_, GELU_, DENSE, KT_, KH_>), grid, block, 0, s, d, a.X,      \
-                       a.stream, a.gdesc, a.walk, a.W, a.bias, a.Y)
+    do {                                                                                          \
+        if (!(KT_) && late)                                                                       \
+            LPV_LAUNCH2(DT_, GELU_, KT_, KH_, !(KT_));                                            \
+        else                                                                                      \
+            LPV_LAUNCH2(DT_, GELU_, KT_, KH_, false);                                             \
+    } while (0)
         // A reduction tail (K = 16 mod 32) only occurs with 16-wide block
         // columns, so the sparse tail kernels are the KH ones.
 #define LPV_LAUNCH(DT_, GELU_)                                                                    \
@@ -999,6 +1026,7 @@ hipError_t launch16(int dtype, bool gelu, Args a, hipStream_t s)
         }
 #undef LPV_LAUNCH
 #undef LPV_LAUNCH1
+#undef LPV_LAUNCH2
         const hipError_t e = hipGetLastError();
         if (e != hipSuccess)
             return e;
