@@ -66,18 +66,18 @@ template <int DT> __device__ inline uint32_t pack2(float a, float b)
 }
 
 // GELU with the error function, x Phi(x), Phi(x) = erfc(-x / sqrt 2) / 2, in
-// float32 without branches.  e = erfc(a), a = |x| / sqrt 2 < 4, is 2^f(a) with
-// f a degree-7 polynomial fitted to log2 erfc on [0, 4] (coefficients from
+// float32 without branches.  erfc(a), a = |x| / sqrt 2 < 4, is 2^f(a) with f
+// a degree-7 polynomial fitted to log2 erfc on [0, 4] (coefficients from
 // gelu_fit.py beside this package's Python files: erfc to 6e-6 relative in
-// float32).  Then x Phi(x) = max(x, 0) - |x| e / 2 for either sign of x (for
-// x < 0 the term |x| e / 2 is the whole result, so the negative tail keeps its
-// relative accuracy): GELU to 5e-6 relative.  From a = 4 on (|x| > 5.65,
-// where |x| erfc(a) / 2 < 5e-8 |x|) the result is max(x, 0); a NaN input gives
-// NaN.
+// float32).  Then x Phi(x) = max(x, 0) - |x| erfc(a) / 2 for either sign of x
+// (for x < 0 that term is the whole result, so the negative tail keeps its
+// relative accuracy), and |x| / 2 = a / sqrt 2, so the term is a e with
+// e = 2^(f(a) - 1/2): one fused multiply-add.  GELU to 5e-6 relative.  From
+// a = 4 on (|x| > 5.65, where |x| erfc(a) / 2 < 5e-8 |x|) the result is
+// max(x, 0); a NaN input gives NaN.
 __device__ inline float gelu_erf(float v)
 {
-    const float ar = fabsf(v) * 0.70710678118654752f;
-    const float a = fminf(ar, 4.0f);
+    const float a = fabsf(v) * 0.70710678118654752f;
     float f = -2.055665755e-05f;
     f = fmaf(f, a, 4.903716035e-04f);
     f = fmaf(f, a, -5.252704490e-03f);
@@ -85,10 +85,10 @@ __device__ inline float gelu_erf(float v)
     f = fmaf(f, a, -1.525942534e-01f);
     f = fmaf(f, a, -9.169431329e-01f);
     f = fmaf(f, a, -1.628112197e+00f);
-    f = fmaf(f, a, 4.628196166e-06f);
-    const float e = __builtin_amdgcn_exp2f(f);  // erfc(a)
+    f = fmaf(f, a, 4.628196166e-06f - 0.5f);
+    const float e = __builtin_amdgcn_exp2f(f);  // erfc(a) / sqrt 2
     const float r = fmaxf(v, 0.0f);
-    return ar >= 4.0f ? r : fmaf(-0.5f, fabsf(v) * e, r);
+    return a >= 4.0f ? r : fmaf(-a, e, r);
 }
 
 // Wave-level inclusive prefix sum over the 64 lanes.

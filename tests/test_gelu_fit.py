@@ -25,12 +25,15 @@ def device_coefficients():
 def gelu32(x, c):
     """The device formula, operation by operation, in float32."""
     x = np.asarray(x, np.float32)
-    ar = (np.abs(x) * np.float32(0.70710678118654752)).astype(np.float32)
-    a = np.minimum(ar, np.float32(4.0))
-    e = np.exp2(gelu_fit.horner32(c, a).astype(np.float64)).astype(np.float32)
-    r = np.maximum(x, np.float32(0.0))
-    t = (np.float32(-0.5) * (np.abs(x) * e).astype(np.float32) + r).astype(np.float32)
-    return np.where(ar >= 4.0, r, t)
+    a = (np.abs(x) * np.float32(0.70710678118654752)).astype(np.float32)
+    c = np.array(c, np.float32)
+    c[0] = np.float32(c[0]) - np.float32(0.5)  # e = 2^(f(a) - 1/2) = erfc(a) / sqrt 2
+    with np.errstate(over="ignore", invalid="ignore"):
+        e = np.exp2(gelu_fit.horner32(c, a).astype(np.float64)).astype(np.float32)
+        r = np.maximum(x, np.float32(0.0))
+        # the fused multiply-add rounds once
+        t = (r.astype(np.float64) - a.astype(np.float64) * e.astype(np.float64)).astype(np.float32)
+    return np.where(a >= 4.0, r, t)
 
 
 def test_device_coefficients_are_the_fit():
